@@ -1,0 +1,413 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these re-type the oracle's own formulas: each compares it with a
+value the paper prints, a closed form the paper prints, an explicit
+construction from the basis definitions, a textbook/library routine, an
+invariant, or brute force on tiny inputs.
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.special
+
+import oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------- measurement
+
+def test_flop_table_matches_paper():
+    """Appendix C.1 table: the three operation counts the paper prints."""
+    with open(os.path.join(GOLDEN, "paper_flop_table.json")) as f:
+        g = json.load(f)
+    s = g["shape_reading"]
+    n = s["N"] // s["block"]
+    p = O.num_coeffs(n, s["frames"])
+    assert p == 845
+    full, conv, solve = O.paper_op_counts(s["N"], s["H"], s["d"], p)
+    pr = g["printed_tflops"]
+    dec = g["printed_decimals"]
+    assert round(full, dec) == pr["full_attention"]
+    assert round(conv, dec) == pr["convert_to_sparsity"]
+    assert round(solve, dec) == pr["solve_kernel"]
+
+
+def test_kept_block_flops_full_mask_is_dense_count():
+    L, bs, d = 1000, 64, 32          # ragged tail of 40 tokens
+    n = O.num_blocks(L, bs)
+    full = [[list(range(n)) for _ in range(n)]]
+    assert O.kept_block_flops(full, L, bs, d) == 4.0 * d * L * L
+
+
+# ---------------------------------------------------------------- a1 pooling
+
+def test_pool_bruteforce_ragged():
+    rng = np.random.default_rng(0)
+    L, d, bs = 150, 5, 64             # blocks of 64, 64, 22
+    x = rng.standard_normal((L, d))
+    got = O.pool(x, bs)
+    assert got.shape == (3, d)
+    for j in range(3):
+        for c in range(d):
+            toks = [x[t, c] for t in range(L) if t // bs == j]
+            assert got[j, c] == pytest.approx(sum(toks) / len(toks), rel=1e-14, abs=1e-15)
+
+
+# ---------------------------------------------------------------- a2 mass
+
+def test_block_mass_aligned_is_softmax_of_block_logits():
+    rng = np.random.default_rng(1)
+    n, d = 12, 8
+    qb, kb = rng.standard_normal((n, d)), rng.standard_normal((n, d))
+    G = O.block_mass(qb, kb, np.full(n, 64), 0.3)
+    ref = scipy.special.softmax(0.3 * qb @ kb.T, axis=1)
+    np.testing.assert_allclose(G, ref, rtol=1e-13, atol=1e-16)
+    np.testing.assert_allclose(G.sum(axis=1), 1.0, rtol=1e-14)
+
+
+def test_block_mass_tail_is_mean_field_token_mass():
+    """With every key token replaced by its block mean, the mass that a
+    query block mean puts on key block j, summed token by token, is G(i, j)."""
+    rng = np.random.default_rng(2)
+    L, bs, d, s = 200, 64, 6, 0.4     # sizes 64, 64, 64, 8
+    q, k = rng.standard_normal((L, d)), rng.standard_normal((L, d))
+    qb, kb = O.pool(q, bs), O.pool(k, bs)
+    G = O.block_mass(qb, kb, O.block_sizes(L, bs), s)
+    n = qb.shape[0]
+    for i in range(n):
+        logit = [s * float(qb[i] @ kb[t // bs]) for t in range(L)]
+        mx = max(logit)
+        w = [math.exp(a - mx) for a in logit]
+        tot = sum(w)
+        for j in range(n):
+            mass = sum(w[t] for t in range(L) if t // bs == j) / tot
+            assert G[i, j] == pytest.approx(mass, rel=1e-12)
+
+
+# ---------------------------------------------------------------- geometry
+
+def test_frame_regions_aligned_and_overlapping():
+    assert O.frame_regions(1024, 64, 256) == [(0, 3), (4, 7), (8, 11), (12, 15)]
+    reg = O.frame_regions(118800, 128, 3600)
+    assert len(reg) == 33 and reg[0] == (0, 28) and reg[1] == (28, 56)
+    assert reg[-1][1] == O.num_blocks(118800, 128) - 1
+    # every 8th frame boundary (8 * 3600 = 225 * 128) is block aligned
+    assert reg[7] == (196, 224) and reg[8] == (225, 253)
+
+
+# ---------------------------------------------------------------- a3 model
+
+CASES = [  # (L, block, frame_tokens)
+    (128, 8, 32),       # n 16, 4 aligned frames
+    (231, 8, 33),       # n 29 with a 7-token tail, 7 frames straddling blocks
+    (240, 10, 48),      # n 24, 5 frames of 4.8 blocks
+    (240, 8, 30),       # n 30, 8 frames of 3.75 blocks
+    (1024, 64, 256),    # the tiny layer: n 16, 4 frames
+    (300, 16, 300),     # a single frame: nullity 2
+]
+
+
+def _case(L, bs, tf):
+    n = O.num_blocks(L, bs)
+    return n, O.frame_regions(L, bs, tf)
+
+
+@pytest.mark.parametrize("L,bs,tf", CASES)
+def test_normal_matrix_equals_explicit(L, bs, tf):
+    n, reg = _case(L, bs, tf)
+    M = O.design_matrix(n, reg)
+    np.testing.assert_array_equal(O.normal_matrix(n, reg), M.T @ M)
+
+
+def test_normal_matrix_blocks_printed_in_paper():
+    """Appendix B.4: C^T C = diag(n-|delta|), D^T D = nI, C^T D is 0/1 with
+    a 1 where the diagonal crosses the column, E^T E = diag(b^2) for frames
+    of b blocks."""
+    n, b = 16, 4
+    reg = O.frame_regions(n * 8, 8, 8 * b)
+    N = O.normal_matrix(n, reg)
+    deltas = np.arange(-(n - 1), n)
+    np.testing.assert_array_equal(np.diag(N)[:2 * n - 1], n - np.abs(deltas))
+    CC = N[:2 * n - 1, :2 * n - 1]
+    np.testing.assert_array_equal(CC, np.diag(np.diag(CC)))
+    np.testing.assert_array_equal(N[2 * n - 1:3 * n - 1, 2 * n - 1:3 * n - 1], n * np.eye(n))
+    CD = N[:2 * n - 1, 2 * n - 1:3 * n - 1]
+    for a, dl in enumerate(deltas):
+        for j in range(n):
+            crosses = any(jj - ii == dl for ii in range(n) for jj in [j])
+            crosses = crosses and 0 <= j - dl < n
+            assert CD[a, j] == (1.0 if crosses else 0.0)
+    np.testing.assert_array_equal(N[3 * n - 1:, 3 * n - 1:], b * b * np.eye(n // b))
+
+
+@pytest.mark.parametrize("L,bs,tf", CASES)
+def test_rhs_equals_explicit(L, bs, tf):
+    n, reg = _case(L, bs, tf)
+    G = np.random.default_rng(3).random((n, n))
+    np.testing.assert_allclose(O.rhs(G, reg), O.design_matrix(n, reg).T @ G.ravel(),
+                               rtol=1e-13)
+
+
+@pytest.mark.parametrize("L,bs,tf", CASES)
+def test_null_space_is_z(L, bs, tf):
+    n, reg = _case(L, bs, tf)
+    M = O.design_matrix(n, reg)
+    sv = np.linalg.svd(M, compute_uv=False)
+    rank = int((sv > sv[0] * 1e-10).sum())
+    F = len(reg)
+    assert rank == M.shape[1] - 1 if F >= 2 else rank == M.shape[1] - 2
+    np.testing.assert_allclose(M @ O.null_vector(n, F), 0.0, atol=1e-12)
+
+
+@pytest.mark.parametrize("L,bs,tf", CASES)
+def test_fit_equals_lstsq_minimum_norm(L, bs, tf):
+    n, reg = _case(L, bs, tf)
+    if len(reg) < 2:
+        pytest.skip("nullity 2")
+    G = np.random.default_rng(4).random((n, n))
+    X = O.fit(G, reg)
+    Xl = O.fit_lstsq(G, reg)
+    np.testing.assert_allclose(X, Xl, rtol=0, atol=1e-10 * np.abs(Xl).max())
+    assert abs(X @ O.null_vector(n, len(reg))) < 1e-10
+
+
+@pytest.mark.parametrize("L,bs,tf", CASES)
+def test_planted_coefficients_recovered(L, bs, tf):
+    n, reg = _case(L, bs, tf)
+    F = len(reg)
+    if F < 2:
+        pytest.skip("nullity 2")
+    rng = np.random.default_rng(5)
+    z = O.null_vector(n, F)
+    Xs = rng.standard_normal(O.num_coeffs(n, F))
+    Xs -= (Xs @ z) / (z @ z) * z
+    G = (O.design_matrix(n, reg) @ Xs).reshape(n, n)
+    np.testing.assert_allclose(O.fit(G, reg), Xs, atol=1e-10)
+    np.testing.assert_allclose(O.reconstruct(Xs, n, reg), G, atol=1e-12)
+
+
+def test_ridge_solution_close_to_minimum_norm():
+    """The paper's Tikhonov lambda = 1e-8 (Appendix B.6) lands within
+    O(lambda) of the minimum-norm solution used here."""
+    n, reg = _case(*CASES[3])
+    G = np.random.default_rng(6).random((n, n))
+    N = O.normal_matrix(n, reg)
+    ridge = np.linalg.solve(N + 1e-8 * np.eye(N.shape[0]), O.rhs(G, reg))
+    X = O.fit(G, reg)
+    assert np.abs(ridge - X).max() < 1e-6 * max(1.0, np.abs(X).max())
+
+
+def test_fit_normal_equations_condition_at_workload_shapes():
+    """The min-norm system stays well conditioned at the layer shapes used."""
+    for L, bs, tf in [(1024, 64, 256), (8192, 128, 1024)]:
+        n, reg = _case(L, bs, tf)
+        N = O.normal_matrix(n, reg)
+        z = O.null_vector(n, len(reg))
+        A = N + (n / (z @ z)) * np.outer(z, z)
+        assert np.linalg.cond(A) < 1e8
+
+
+# ---------------------------------------------------------------- a4 prediction
+
+def test_extrapolation_reproduces_linear_sequences():
+    rng = np.random.default_rng(7)
+    n, F = 6, 2
+    a, b = rng.standard_normal(O.num_coeffs(n, F)), rng.standard_normal(O.num_coeffs(n, F))
+    X = lambda t: a + b * t  # noqa: E731
+    for t1, t2, t in [(4, 5, 9), (5, 15, 22), (10, 20, 20), (3, 7, 5)]:
+        c, d = O.extrapolate(X(t1), t1, X(t2), t2, t, n)
+        cs, ds, _ = O.split_coeffs(X(t), n)
+        np.testing.assert_allclose(c, cs, atol=1e-12)
+        np.testing.assert_allclose(d, ds, atol=1e-12)
+
+
+def test_gauge_invariance_of_scores():
+    rng = np.random.default_rng(8)
+    n, F = 9, 3
+    X = rng.standard_normal(O.num_coeffs(n, F))
+    z = O.null_vector(n, F)
+    for alpha in (0.3, -2.0):
+        c1, d1, _ = O.split_coeffs(X, n)
+        c2, d2, _ = O.split_coeffs(X + alpha * z, n)
+        np.testing.assert_allclose(O.scores(c1, d1, n), O.scores(c2, d2, n), atol=1e-12)
+
+
+def test_gate_reading():
+    assert O.gate([np.array([0.1, 0.3]), np.array([0.2, 0.05])], 0.0)
+    assert not O.gate([np.array([0.1, 0.3]), np.array([-0.2, 0.05])], 0.0)
+    assert not O.gate([np.array([0.4])], 0.5)
+
+
+# ---------------------------------------------------------------- a5 selection
+
+def test_pattern_index_convention_picks_the_planted_diagonal_and_column():
+    """Fit a map that is one parallel diagonal (j - i = +3) plus one strong
+    column: the top-2 selection of every row must be exactly those."""
+    n, bs = 16, 8
+    reg = O.frame_regions(n * bs, bs, n * bs // 2)
+    G = 0.01 * O.basis_C(n, 3) + 0.05 * O.basis_D(n, 11) + 0.001
+    X = O.fit(G, reg)
+    c, d, _ = O.split_coeffs(X, n)
+    sig = O.scores(c, d, n)
+    forced = O.forced_mask(n, reg, False)
+    for i, r in enumerate(O.select(sig, forced, "topk", density=2 / n)):
+        want = {11} | ({i + 3} if i + 3 < n else set())
+        if len(want) == 1:
+            assert 11 in set(r.kept.tolist())
+        else:
+            assert set(r.kept.tolist()) == want
+
+
+def test_topk_count():
+    assert O.topk_count(0.30, 16) == 5
+    assert O.topk_count(0.25, 64) == 16
+    assert O.topk_count(0.05, 591) == 30
+    assert O.topk_count(0.10, 591) == 60
+    assert O.topk_count(0.5, 591) == 296
+    assert O.topk_count(1.0, 929) == 929
+    assert O.topk_count(1e-9, 929) == 1
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_topk_row_bruteforce(seed):
+    rng = np.random.default_rng(100 + seed)
+    n = 9
+    sig = rng.standard_normal(n)
+    forced = rng.random(n) < 0.25
+    k = int(rng.integers(1, n + 1))
+    got = set(O.select_row_topk(sig, forced, k).kept.tolist())
+    free = [j for j in range(n) if not forced[j]]
+    kk = min(len(free), max(0, k - int(forced.sum())))
+    best = max(itertools.combinations(free, kk), key=lambda s: sum(sig[j] for j in s))
+    assert got == set(best) | set(np.flatnonzero(forced).tolist())
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_mass_row_bruteforce(seed):
+    """The kept set is a smallest set (with the forced blocks) whose positive
+    mass reaches tau, and among those the heaviest."""
+    rng = np.random.default_rng(200 + seed)
+    n = 9
+    sig = rng.standard_normal(n) + 0.5
+    forced = rng.random(n) < 0.2
+    tau = float(rng.uniform(0.3, 0.95))
+    got = O.select_row_mass(sig, forced, tau)
+    pos = np.maximum(sig.astype(np.float32).astype(np.float64), 0)
+    target = np.float32(tau) * pos.sum()
+    fset = set(np.flatnonzero(forced).tolist())
+    free = [j for j in range(n) if not forced[j]]
+    fm = sum(pos[j] for j in fset)
+    for size in range(0 if fset else 1, len(free) + 1):
+        ok = [s for s in itertools.combinations(free, size) if fm + sum(pos[j] for j in s) >= target]
+        if ok:
+            best = max(ok, key=lambda s: sum(pos[j] for j in s))
+            break
+    assert set(got.kept.tolist()) == set(best) | fset
+    assert sum(pos[j] for j in got.kept) >= target
+
+
+def test_mass_row_zero_mass_keeps_one_block():
+    r = O.select_row_mass(-np.ones(6), np.zeros(6, bool), 0.9)
+    assert r.kept.tolist() == [0]
+
+
+def test_selection_ties_break_by_index():
+    r = O.select_row_topk(np.ones(8), np.zeros(8, bool), 3)
+    assert r.kept.tolist() == [0, 1, 2] and r.key_gap == 0.0
+
+
+# ---------------------------------------------------------------- a6 attention
+
+def test_full_mask_equals_textbook_attention():
+    rng = np.random.default_rng(9)
+    L, d, bs = 200, 16, 64
+    q, k, v = (rng.standard_normal((L, d)) for _ in range(3))
+    n = O.num_blocks(L, bs)
+    Ob, lse = O.attention(q, k, v, [list(range(n))] * n, bs, 1 / math.sqrt(d))
+    A = q @ k.T / math.sqrt(d)
+    np.testing.assert_allclose(Ob, scipy.special.softmax(A, axis=1) @ v, atol=1e-12)
+    np.testing.assert_allclose(lse, scipy.special.logsumexp(A, axis=1), atol=1e-12)
+
+
+def test_outputs_are_convex_combinations_of_kept_values():
+    """With V = identity the output row is the attention distribution:
+    non-negative, summing to one, zero outside the kept blocks."""
+    rng = np.random.default_rng(10)
+    L, d, bs = 96, 8, 16
+    q, k = rng.standard_normal((L, d)), rng.standard_normal((L, d))
+    n = O.num_blocks(L, bs)
+    lists = [sorted(rng.choice(n, size=int(rng.integers(1, n + 1)), replace=False).tolist())
+             for _ in range(n)]
+    P, _ = O.attention(q, k, np.eye(L), lists, bs, 0.5)
+    assert (P >= 0).all()
+    np.testing.assert_allclose(P.sum(axis=1), 1.0, atol=1e-12)
+    for i in range(n):
+        allowed = np.zeros(L, bool)
+        for j in lists[i]:
+            allowed[j * bs:(j + 1) * bs] = True
+        assert (P[i * bs:(i + 1) * bs][:, ~allowed] == 0).all()
+
+
+def test_single_block_bruteforce():
+    rng = np.random.default_rng(11)
+    L, d, bs = 40, 3, 16                 # blocks 16, 16, 8
+    q, k, v = (rng.standard_normal((L, d)) for _ in range(3))
+    lists = [[2], [0], [1]]
+    Ob, lse = O.attention(q, k, v, lists, bs, 0.7)
+    for p in range(L):
+        j = lists[p // bs][0]
+        keys = range(j * bs, min(L, (j + 1) * bs))
+        logits = [0.7 * sum(q[p, c] * k[t, c] for c in range(d)) for t in keys]
+        mx = max(logits)
+        w = [math.exp(a - mx) for a in logits]
+        s = sum(w)
+        for c in range(d):
+            want = sum(wi * v[t, c] for wi, t in zip(w, keys)) / s
+            assert Ob[p, c] == pytest.approx(want, abs=1e-12)
+        assert lse[p] == pytest.approx(mx + math.log(s), abs=1e-12)
+
+
+def test_empty_list_gives_zero_output():
+    q = np.ones((8, 2))
+    Ob, lse = O.attention(q, q, q, [[], [0]], 4, 1.0)
+    assert (Ob[:4] == 0).all() and np.isneginf(lse[:4]).all()
+
+
+# ---------------------------------------------------------------- predictor
+
+def test_predictor_schedule_and_errors():
+    rng = np.random.default_rng(12)
+    B, H, L, d, bs, tf = 1, 1, 256, 8, 32, 64
+    q, k = rng.standard_normal((B, H, L, d)), rng.standard_normal((B, H, L, d))
+    P = O.Predictor(B, H, L, d, bs, tf, warmup_m=2, delta_t=3)
+    with pytest.raises(ValueError):
+        P.predict(q, k, 3, O.Budget("topk", 0.5))
+    P.collect(q, k, 1)
+    P.collect(q, k, 2)
+    with pytest.raises(ValueError):
+        P.collect(q, k, 2)
+    assert [t for t in range(3, 12) if P.is_anchor_step(t)] == [5, 8, 11]
+    P1 = O.Predictor(B, H, L, d, bs, tf, warmup_m=2, delta_t=3, anchor_rule=1)
+    assert [t for t in range(3, 12) if P1.is_anchor_step(t)] == [3, 6, 9]
+    out = P.predict(q, k, 3, O.Budget("topk", 0.5))
+    n = O.num_blocks(L, bs)
+    assert all(len(r.kept) >= O.topk_count(0.5, n) for r in out[0][0])
+
+
+def test_predictor_identical_steps_give_identical_masks():
+    """Two identical anchors extrapolate to themselves (zero slope)."""
+    rng = np.random.default_rng(13)
+    q, k = rng.standard_normal((1, 2, 256, 8)), rng.standard_normal((1, 2, 256, 8))
+    P = O.Predictor(1, 2, 256, 8, 32, 64, warmup_m=2, delta_t=0)
+    P.collect(q, k, 1)
+    P.collect(q, k, 2)
+    a = P.predict(q, k, 3, O.Budget("mass", mass=0.8))
+    b = P.predict(q, k, 9, O.Budget("mass", mass=0.8))
+    for h in range(2):
+        for ra, rb in zip(a[0][h], b[0][h]):
+            assert ra.kept.tolist() == rb.kept.tolist()
