@@ -1,0 +1,185 @@
+/*
+ * moddit.h -- C ABI of the MI355X (gfx950) MOD-DiT hot path.
+ *
+ * MOD-DiT (arXiv 2601.11641) predicts, for every attention head and every
+ * query block of a video-DiT attention layer, which key/value blocks to keep,
+ * from a mixture-of-distributions (MOD) linear model of the block-level
+ * attention statistic (Section 4.2, Eq. 3/Eq. 4) fitted at early denoising
+ * steps and extrapolated linearly across steps (Section 5.2), and then runs
+ * attention over the kept blocks only (Eq. 1).  This library implements that
+ * path on one GPU:
+ *
+ *   mod_collect_stats        dense warm-up step: pool Q/K per block, build the
+ *                            pooled block-mass statistic G, fit the MOD
+ *                            coefficients X = [c, d, e] (Eq. 4, min-norm)
+ *   mod_predict_block_mask   sparse step: optionally re-anchor (fit again),
+ *                            extrapolate c and d (Section 5.2), score blocks and
+ *                            select per query block (Section 5.3)
+ *   mod_block_sparse_attn_fwd  softmax attention over the kept blocks (Eq. 1)
+ *
+ * Conventions shared by every entry point
+ *   - Q, K, V, O are bfloat16, contiguous [B, H, L, d] (d fastest), device
+ *     memory owned by the caller, 16-byte aligned.  L is the token count and
+ *     d the head dimension; blocks are `block` consecutive tokens, the last
+ *     block may be short (n = ceil(L / block) blocks).
+ *   - Tokens are frame-first; `frame_tokens` tokens make one latent frame and
+ *     each frame defines one block-diagonal region (Appendix B.3).
+ *   - Supported: d in {64, 128}, block in {64, 128}, 2 <= L / frame_tokens,
+ *     L % frame_tokens == 0, n <= 4096.  Other shapes: MOD_ERR_UNSUPPORTED.
+ *   - Every call is asynchronous on `stream` (a hipStream_t; NULL is the
+ *     default stream) unless stated otherwise.  Arguments are validated on
+ *     the host before anything is enqueued; on error nothing is enqueued and
+ *     mod_last_error() holds a message (thread-local).
+ *   - No exception crosses the ABI and nothing aborts.
+ *   - A mod_stats handle is used by one thread and one stream at a time.
+ */
+#ifndef MODDIT_H
+#define MODDIT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MOD_OK = 0,
+    MOD_ERR_INVALID_ARG = 1,   /* null pointer, non-positive size, bad budget   */
+    MOD_ERR_UNSUPPORTED = 2,   /* shape outside the supported set                */
+    MOD_ERR_BAD_STATE = 3,     /* step order / predict before any collected step */
+    MOD_ERR_HIP = 4,           /* HIP runtime or kernel-launch error             */
+    MOD_ERR_NOMEM = 5          /* device or host allocation failed               */
+} mod_status;
+
+/* Shape of one attention layer. */
+typedef struct {
+    int B;             /* batch                                  */
+    int H;             /* heads                                  */
+    int L;             /* tokens per sequence                    */
+    int d;             /* head dimension                         */
+    int block;         /* tokens per block (the paper's B)       */
+    int frame_tokens;  /* tokens per latent frame                */
+} mod_shape;
+
+/* Predictor schedule (Algorithm 1 hyper-parameters). */
+typedef struct {
+    int warmup_m;      /* m: dense warm-up steps (Section 5)                 */
+    int delta_t;       /* re-anchor interval; <= 0 never re-anchors          */
+    float tau_e;       /* block-diagonal threshold (Section 5.3)            */
+    int anchor_rule;   /* 0: re-anchor at t = m + i*delta_t, i >= 1 (the
+                          prediction steps of Section 5); 1: at t % delta_t == 0
+                          (Algorithm 1)                                      */
+} mod_params;
+
+typedef enum { MOD_BUDGET_TOPK = 0, MOD_BUDGET_MASS = 1 } mod_budget_mode;
+
+/* Per-row sparsity budget.
+ *   TOPK: keep k = clamp(ceil(density * n - 1e-6), 1, n) blocks per query
+ *         block (density taken at float precision), the forced block-diagonal
+ *         blocks counted first.
+ *   MASS: keep the forced blocks plus the shortest score-ordered prefix of
+ *         the others whose positive score mass reaches `mass` of the row's
+ *         total positive mass (at least one block). */
+typedef struct {
+    int mode;          /* mod_budget_mode            */
+    float density;     /* TOPK: in (0, 1]            */
+    float mass;        /* MASS: in (0, 1]            */
+} mod_budget;
+
+typedef struct mod_stats mod_stats;   /* opaque, library-owned */
+
+/* n = ceil(L / block); 0 for a null or invalid shape. */
+int mod_num_blocks(const mod_shape* shape);
+
+/* |X| = 3n - 1 + F coefficients per head (Eq. 4: 2n-1 diagonals, n
+ * verticals, F = L / frame_tokens frame regions); 0 if invalid. */
+int mod_num_coeffs(const mod_shape* shape);
+
+/* Create the predictor state of one layer.  Builds, on the host in fp64, the
+ * closed-form normal matrix of the MOD least-squares problem (Appendix B.4)
+ * reduced to its Schur complement, factors and inverts it once, allocates
+ * the device buffers and uploads the tables.  Synchronous.  On success *out
+ * owns about (2*B*H*n*d + B*H*n*n + 8*B*H*n) * 8 bytes of device memory. */
+mod_status mod_stats_create(const mod_shape* shape, const mod_params* params,
+                            mod_stats** out);
+
+/* Release the handle and its device memory (waits for the device).  NULL is
+ * accepted. */
+mod_status mod_stats_destroy(mod_stats* stats);
+
+/* Dense warm-up step `step` (Algorithm 1, warm-up phase): fit the MOD
+ * coefficients (Eq. 4) on the pooled block-mass statistic of q, k
+ * ([B,H,L,d] bf16 device pointers) and record (step, X) as the newest of the
+ * two anchors kept.  Steps must strictly increase across collect and
+ * predict calls (else MOD_ERR_BAD_STATE). */
+mod_status mod_collect_stats(mod_stats* stats, const void* q, const void* k, int step,
+                             void* stream);
+
+/* Sparse step `step` (Algorithm 1, main phase; Sections 5.2-5.3).
+ * On the first call the block-diagonal gate of every head is fixed from the
+ * anchors held (gate on iff min over anchors of mean_f e_f > tau_e).  If
+ * `step` is a re-anchor step, q and k are pooled and fitted first (else they
+ * are not read and may be NULL).  Then c and d are extrapolated to `step`
+ * from the two newest anchors (zero slope with one anchor) and every query
+ * block i of every head selects key blocks by the score
+ *   sigma(i, j) = n * (c~[j - i] + d~[j])
+ * ranked at float precision, ties to the smaller j, the frame blocks of i
+ * forced in when the gate is on.
+ * Output (device, caller-owned):
+ *   kv_idx [B, H, n, n] int32: row (b,h,i) starts at ((b*H+h)*n+i)*n and
+ *          holds kv_cnt[(b*H+h)*n+i] ascending block indices; the rest of
+ *          the row is not written.
+ *   kv_cnt [B, H, n] int32, in [1, n].
+ * Requires at least one collected step (else MOD_ERR_BAD_STATE). */
+mod_status mod_predict_block_mask(mod_stats* stats, const void* q, const void* k, int step,
+                                  const mod_budget* budget, int32_t* kv_idx, int32_t* kv_cnt,
+                                  void* stream);
+
+/* Device workspace the attention call needs (bytes; 0 means none). */
+size_t mod_attn_workspace_bytes(const mod_shape* shape);
+
+/* Block-sparse attention forward (Eq. 1 with the block mask of the lists):
+ * for every query token p of block i of head (b,h),
+ *   O_p = sum over tokens q of the kept blocks of softmax_q(scale * Q_p.K_q) V_q
+ *   lse_p = log sum_q exp(scale * Q_p.K_q)        (natural log)
+ * with the kept blocks kv_idx[row][0 .. kv_cnt[row]) (layout of
+ * mod_predict_block_mask; indices in [0, n), each at most once).  A row with
+ * kv_cnt = 0 gives O = 0 and lse = -inf.  scale = 0 means 1/sqrt(d).
+ * q, k, v, o: [B,H,L,d] bf16 device; lse: [B,H,L] fp32 device or NULL.
+ * bf16 MFMA products, fp32 softmax and accumulation.  `frame_tokens` of the
+ * shape is not used.  workspace may be NULL when mod_attn_workspace_bytes
+ * returns 0. */
+mod_status mod_block_sparse_attn_fwd(const mod_shape* shape, const void* q, const void* k,
+                                     const void* v, const int32_t* kv_idx,
+                                     const int32_t* kv_cnt, float scale, void* o, float* lse,
+                                     void* workspace, size_t ws_bytes, void* stream);
+
+/* ---- introspection (synchronous copies to host memory; for tests) ---- */
+
+/* Anchor `slot` (0 = newest, 1 = the one before): coefficients
+ * [B, H, 3n-1+F] fp64 (order c_{-(n-1)..n-1}, d_{0..n-1}, e_{0..F-1};
+ * minimum-norm gauge) and its step.  MOD_ERR_BAD_STATE if absent. */
+mod_status mod_stats_get_anchor(const mod_stats* stats, int slot, double* host_coeffs,
+                                int* step);
+
+/* Block means of the last fitted q, k: [B, H, n, d] fp64 each. */
+mod_status mod_stats_get_pooled(const mod_stats* stats, double* host_qbar, double* host_kbar);
+
+/* Pooled block-mass statistic G of the last fit: [B, H, n, n] fp64. */
+mod_status mod_stats_get_block_mass(const mod_stats* stats, double* host_G);
+
+/* Last prediction (c~, d~): [B, H, 3n-1] fp64. */
+mod_status mod_stats_get_prediction(const mod_stats* stats, double* host_pred);
+
+/* Block-diagonal gate per head, [B, H] int32 (0/1); MOD_ERR_BAD_STATE
+ * before the first predict. */
+mod_status mod_stats_get_gate(const mod_stats* stats, int32_t* host_gate);
+
+const char* mod_status_string(mod_status status);
+const char* mod_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MODDIT_H */

@@ -1,0 +1,51 @@
+// Internal launch interface of the MOD-DiT gfx950 kernels.  Every launcher
+// enqueues on `s` and returns the launch status; shapes are validated by the
+// C ABI layer before any launcher is called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace moddit {
+
+constexpr int kMaxBlocks = 4096;     // largest n (selection keeps a row in LDS)
+
+// a1: block means of Q and K, fp64 [BH, n, d].
+hipError_t launch_pool(const uint16_t* q, const uint16_t* k, double* qbar, double* kbar,
+                       int BH, int L, int d, int bs, int n, hipStream_t s);
+
+// a2: pooled block-mass statistic G [BH, n, n] fp64 (row-stochastic).
+hipError_t launch_block_mass(const double* qbar, const double* kbar, double* G, int BH,
+                             int L, int d, int bs, int n, double scale, hipStream_t s);
+
+// a3: right-hand side M^T vec(G) [BH, p] and the structured minimum-norm
+// solve into X [BH, p].  reg: [F][2] inclusive block ranges; Sinv: inverse
+// of the Schur complement [q, q], q = n - 1 + F; bU, u: scratch [BH, q].
+hipError_t launch_rhs(const double* G, const int* reg, double* r, int BH, int n, int F,
+                      hipStream_t s);
+hipError_t launch_solve(const double* r, const int* reg, const double* Sinv, double* bU,
+                        double* u, double* X, int BH, int n, int F, hipStream_t s);
+
+// Block-diagonal gate per head from one or two anchors (Xb may equal Xa).
+hipError_t launch_gate(const double* Xa, const double* Xb, int32_t* gate, int BH, int n,
+                       int F, double tau_e, hipStream_t s);
+
+// a4: pred [BH, 3n-1] = x2 + (x2 - x1) * w over the c and d parts.
+hipError_t launch_extrapolate(const double* X1, const double* X2, double w, double* pred,
+                              int BH, int n, int F, hipStream_t s);
+
+// a5: per-row selection into compacted lists.  row_lo/row_hi: union of the
+// frame regions holding block i; mode 0 = TOPK (k), 1 = MASS (tau).
+hipError_t launch_select(const double* pred, const int32_t* gate, const int* row_lo,
+                         const int* row_hi, int mode, int k, double tau, int32_t* kv_idx,
+                         int32_t* kv_cnt, int BH, int n, hipStream_t s);
+
+// a6: block-sparse attention forward.
+hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                           const int32_t* kv_idx, const int32_t* kv_cnt, float scale,
+                           uint16_t* o, float* lse, int BH, int L, int d, int bs, int n,
+                           hipStream_t s);
+
+}  // namespace moddit

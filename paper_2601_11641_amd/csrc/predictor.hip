@@ -1,0 +1,587 @@
+// Mask predictor kernels for gfx950 (wave64).
+//
+// All predictor arithmetic is fp64: the block sums of bf16 values are exact
+// in fp64, and the statistic, the fit and the scores then agree with an fp64
+// reference to rounding level, so the integer outcome (which blocks are kept)
+// only depends on the float32 ranking keys.  Every reduction runs in a fixed
+// order (no floating-point atomics), so results are bitwise reproducible.
+//
+// Paper references: block pooling + mass estimate stand in for the sparsity
+// map of Eq. 2; the fit solves the normal equations of Eq. 4 with the block
+// structure of Appendix B.4; the prediction is the linear extrapolation of
+// Section 5.2; the selection implements the ranking and the gated
+// block-diagonal support of Section 5.3.
+#include "moddit_internal.h"
+
+#include <cmath>
+
+namespace moddit {
+namespace {
+
+constexpr int kThreads = 256;
+
+__device__ inline double bf16_bits_to_double(uint32_t bits) {
+    return static_cast<double>(__uint_as_float(bits << 16));
+}
+
+// Fixed-order tree reductions over one 256-thread workgroup.
+__device__ double block_sum(double v, double* red) {
+    red[threadIdx.x] = v;
+    __syncthreads();
+    for (int s = kThreads / 2; s > 0; s >>= 1) {
+        if (threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+        __syncthreads();
+    }
+    double r = red[0];
+    __syncthreads();
+    return r;
+}
+
+__device__ double block_max(double v, double* red) {
+    red[threadIdx.x] = v;
+    __syncthreads();
+    for (int s = kThreads / 2; s > 0; s >>= 1) {
+        if (threadIdx.x < s) red[threadIdx.x] = fmax(red[threadIdx.x], red[threadIdx.x + s]);
+        __syncthreads();
+    }
+    double r = red[0];
+    __syncthreads();
+    return r;
+}
+
+// ---------------------------------------------------------------------------
+// a1: block pooling.  Grid (n, BH, 2): z = 0 pools Q, z = 1 pools K.  The
+// block is one contiguous run of rows*D bf16; each thread reads 16-byte
+// chunks of a fixed channel group on every R-th row and accumulates in fp64.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(kThreads) void pool_kernel(const uint16_t* __restrict__ q,
+                                                        const uint16_t* __restrict__ k,
+                                                        double* __restrict__ qbar,
+                                                        double* __restrict__ kbar, int L,
+                                                        int bs, int n) {
+    constexpr int C = D / 8;        // 16-byte chunks per row
+    constexpr int R = kThreads / C; // rows per pass
+    __shared__ double part[R][D + 1];
+    const int i = blockIdx.x, bh = blockIdx.y;
+    const uint16_t* src = (blockIdx.z == 0 ? q : k) + ((size_t)bh * L + (size_t)i * bs) * D;
+    double* dst = (blockIdx.z == 0 ? qbar : kbar) + ((size_t)bh * n + i) * D;
+    const int cnt = min(bs, L - i * bs);
+    const int t = threadIdx.x, c = t % C, r0 = t / C;
+    double acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+    for (int r = r0; r < cnt; r += R) {
+        const uint4 w = *reinterpret_cast<const uint4*>(src + (size_t)r * D + c * 8);
+        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            acc[2 * e] += bf16_bits_to_double(ws[e] & 0xFFFFu);
+            acc[2 * e + 1] += bf16_bits_to_double(ws[e] >> 16);
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) part[r0][c * 8 + e] = acc[e];
+    __syncthreads();
+    if (t < D) {
+        double s = 0.0;
+        for (int r = 0; r < R; ++r) s += part[r][t];
+        dst[t] = s / static_cast<double>(cnt);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// a2 (part 1): block logits scale * qbar_i . kbar_j, 64 x 64 tile per
+// workgroup, 4 x 4 outputs per thread, channels staged through LDS.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(kThreads) void logits_kernel(const double* __restrict__ qbar,
+                                                          const double* __restrict__ kbar,
+                                                          double* __restrict__ G, int n,
+                                                          double scale) {
+    constexpr int T = 64, KC = 16;
+    __shared__ double qs[T][KC + 1];
+    __shared__ double ks[T][KC + 1];
+    const int bh = blockIdx.z, i0 = blockIdx.y * T, j0 = blockIdx.x * T;
+    const double* qb = qbar + (size_t)bh * n * D;
+    const double* kb = kbar + (size_t)bh * n * D;
+    const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+    double acc[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
+    for (int d0 = 0; d0 < D; d0 += KC) {
+        for (int e = threadIdx.x; e < T * KC; e += kThreads) {
+            const int r = e / KC, c = e % KC;
+            qs[r][c] = (i0 + r < n) ? qb[(size_t)(i0 + r) * D + d0 + c] : 0.0;
+            ks[r][c] = (j0 + r < n) ? kb[(size_t)(j0 + r) * D + d0 + c] : 0.0;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < KC; ++c) {
+            double a[4], b[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                a[u] = qs[ty + 16 * u][c];
+                b[u] = ks[tx + 16 * u][c];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) acc[u][v] = fma(a[u], b[v], acc[u][v]);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int i = i0 + ty + 16 * u;
+        if (i >= n) continue;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int j = j0 + tx + 16 * v;
+            if (j < n) G[((size_t)bh * n + i) * n + j] = scale * acc[u][v];
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// a2 (part 2): G(i, j) = |j| exp(l_ij - max_j l) / sum_j |j| exp(...), one
+// workgroup per (head, row), in place.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void mass_softmax_kernel(double* __restrict__ G, int L,
+                                                                int bs, int n) {
+    __shared__ double red[kThreads];
+    double* g = G + (size_t)blockIdx.x * n;
+    double m = -INFINITY;
+    for (int j = threadIdx.x; j < n; j += kThreads) m = fmax(m, g[j]);
+    m = block_max(m, red);
+    double s = 0.0;
+    for (int j = threadIdx.x; j < n; j += kThreads) {
+        const double w = static_cast<double>(min(bs, L - j * bs)) * exp(g[j] - m);
+        g[j] = w;
+        s += w;
+    }
+    s = block_sum(s, red);
+    for (int j = threadIdx.x; j < n; j += kThreads) g[j] = g[j] / s;
+}
+
+// ---------------------------------------------------------------------------
+// a3 (rhs): r = M^T vec(G): diagonal sums (2n-1), column sums (n) and frame
+// square sums (F).  One thread per output, sequential in-order sums; the
+// diagonal and column loops read consecutive addresses across threads.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void rhs_kernel(const double* __restrict__ G,
+                                                       const int* __restrict__ reg,
+                                                       double* __restrict__ r, int n, int F) {
+    const int bh = blockIdx.y;
+    const int o = blockIdx.x * kThreads + threadIdx.x;
+    const int p = 3 * n - 1 + F;
+    if (o >= p) return;
+    const double* g = G + (size_t)bh * n * n;
+    double s = 0.0;
+    if (o < 2 * n - 1) {
+        const int dl = o - (n - 1);
+        const int i0 = max(0, -dl), i1 = min(n - 1, n - 1 - dl);
+        for (int i = i0; i <= i1; ++i) s += g[(size_t)i * n + i + dl];
+    } else if (o < 3 * n - 1) {
+        const int j = o - (2 * n - 1);
+        for (int i = 0; i < n; ++i) s += g[(size_t)i * n + j];
+    } else {
+        const int f = o - (3 * n - 1);
+        const int lo = reg[2 * f], hi = reg[2 * f + 1];
+        for (int i = lo; i <= hi; ++i)
+            for (int j = lo; j <= hi; ++j) s += g[(size_t)i * n + j];
+    }
+    r[(size_t)bh * p + o] = s;
+}
+
+// ---------------------------------------------------------------------------
+// a3 (solve).  The normal matrix N = M^T M has a diagonal C^T C block
+// (Appendix B.4).  Fixing the gauge by dropping the last vertical column,
+// the unknowns split into c (2n-1) and u = [d_0..d_{n-2}, e] (q = n-1+F):
+//   [Dc  W ] [c]   [r_C]          S = Y - W^T Dc^{-1} W   (host, inverted)
+//   [W^T Y ] [u] = [r_U],         u = S^{-1} (r_U - W^T Dc^{-1} r_C)
+//                                 c = Dc^{-1} (r_C - W u)
+// with Dc = diag(n - |delta|), W[delta, j] = 1 iff column j crosses
+// diagonal delta, W[delta, f] = max(0, |R_f| - |delta|).  The result is
+// moved to the minimum-norm gauge by removing its component along
+// z = [1, -1, 0].
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void solve_pre_kernel(const double* __restrict__ r,
+                                                             const int* __restrict__ reg,
+                                                             double* __restrict__ bU, int n,
+                                                             int F) {
+    extern __shared__ double y[];   // 2n - 1
+    const int bh = blockIdx.x;
+    const int p = 3 * n - 1 + F, q = n - 1 + F;
+    const double* rr = r + (size_t)bh * p;
+    for (int a = threadIdx.x; a < 2 * n - 1; a += kThreads)
+        y[a] = rr[a] / static_cast<double>(n - abs(a - (n - 1)));
+    __syncthreads();
+    for (int j = threadIdx.x; j < q; j += kThreads) {
+        double s = 0.0, b;
+        if (j < n - 1) {
+            for (int a = j; a <= j + n - 1; ++a) s += y[a];
+            b = rr[2 * n - 1 + j];
+        } else {
+            const int f = j - (n - 1);
+            const int sz = reg[2 * f + 1] - reg[2 * f] + 1;
+            for (int dl = -(sz - 1); dl <= sz - 1; ++dl)
+                s += static_cast<double>(sz - abs(dl)) * y[dl + n - 1];
+            b = rr[3 * n - 1 + f];
+        }
+        bU[(size_t)bh * q + j] = b - s;
+    }
+}
+
+// u[h] = S^{-1} bU[h] for all heads; S^{-1} symmetric, read row-wise so that
+// consecutive threads read consecutive addresses.
+__global__ __launch_bounds__(kThreads) void solve_gemv_kernel(const double* __restrict__ Sinv,
+                                                              const double* __restrict__ bU,
+                                                              double* __restrict__ u, int q,
+                                                              int BH) {
+    constexpr int HB = 4, KT = 1024;
+    __shared__ double bs[HB][KT];
+    const int j = blockIdx.x * kThreads + threadIdx.x;
+    const int h0 = blockIdx.y * HB;
+    double acc[HB];
+#pragma unroll
+    for (int hh = 0; hh < HB; ++hh) acc[hh] = 0.0;
+    for (int k0 = 0; k0 < q; k0 += KT) {
+        const int kt = min(KT, q - k0);
+        for (int e = threadIdx.x; e < HB * KT; e += kThreads) {
+            const int hh = e / KT, kk = e % KT;
+            bs[hh][kk] = (h0 + hh < BH && kk < kt) ? bU[(size_t)(h0 + hh) * q + k0 + kk] : 0.0;
+        }
+        __syncthreads();
+        if (j < q) {
+            for (int kk = 0; kk < kt; ++kk) {
+                const double a = Sinv[(size_t)(k0 + kk) * q + j];
+#pragma unroll
+                for (int hh = 0; hh < HB; ++hh) acc[hh] = fma(a, bs[hh][kk], acc[hh]);
+            }
+        }
+        __syncthreads();
+    }
+    if (j < q) {
+#pragma unroll
+        for (int hh = 0; hh < HB; ++hh)
+            if (h0 + hh < BH) u[(size_t)(h0 + hh) * q + j] = acc[hh];
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void solve_post_kernel(const double* __restrict__ r,
+                                                              const double* __restrict__ u,
+                                                              const int* __restrict__ reg,
+                                                              double* __restrict__ X, int n,
+                                                              int F) {
+    extern __shared__ double us[];   // q
+    __shared__ double red[kThreads];
+    const int bh = blockIdx.x;
+    const int p = 3 * n - 1 + F, q = n - 1 + F;
+    for (int a = threadIdx.x; a < q; a += kThreads) us[a] = u[(size_t)bh * q + a];
+    __syncthreads();
+    const double* rr = r + (size_t)bh * p;
+    double* x = X + (size_t)bh * p;
+    double part = 0.0;   // sum(c) - sum(d) of this thread's entries
+    for (int a = threadIdx.x; a < 2 * n - 1; a += kThreads) {
+        const int dl = a - (n - 1);
+        double s = 0.0;
+        const int j0 = max(0, dl), j1 = min(n - 2, dl + n - 1);
+        for (int j = j0; j <= j1; ++j) s += us[j];
+        for (int f = 0; f < F; ++f) {
+            const int w = (reg[2 * f + 1] - reg[2 * f] + 1) - abs(dl);
+            if (w > 0) s += static_cast<double>(w) * us[n - 1 + f];
+        }
+        const double c = (rr[a] - s) / static_cast<double>(n - abs(dl));
+        x[a] = c;
+        part += c;
+    }
+    for (int j = threadIdx.x; j < n; j += kThreads) {
+        const double dj = (j < n - 1) ? us[j] : 0.0;
+        x[2 * n - 1 + j] = dj;
+        part -= dj;
+    }
+    for (int f = threadIdx.x; f < F; f += kThreads) x[3 * n - 1 + f] = us[n - 1 + f];
+    const double alpha = block_sum(part, red) / static_cast<double>(3 * n - 1);
+    for (int a = threadIdx.x; a < 2 * n - 1; a += kThreads) x[a] -= alpha;
+    for (int j = threadIdx.x; j < n; j += kThreads) x[2 * n - 1 + j] += alpha;
+}
+
+// ---------------------------------------------------------------------------
+// Gate: on iff min over the anchors of the frame-averaged e exceeds tau_e.
+// ---------------------------------------------------------------------------
+__global__ void gate_kernel(const double* __restrict__ Xa, const double* __restrict__ Xb,
+                            int32_t* __restrict__ gate, int BH, int n, int F, double tau_e) {
+    const int bh = blockIdx.x * blockDim.x + threadIdx.x;
+    if (bh >= BH) return;
+    const int p = 3 * n - 1 + F;
+    double ea = 0.0, eb = 0.0;
+    for (int f = 0; f < F; ++f) {
+        ea += Xa[(size_t)bh * p + 3 * n - 1 + f];
+        eb += Xb[(size_t)bh * p + 3 * n - 1 + f];
+    }
+    ea /= F;
+    eb /= F;
+    gate[bh] = fmin(ea, eb) > tau_e ? 1 : 0;
+}
+
+// ---------------------------------------------------------------------------
+// a4: linear extrapolation of c and d (Section 5.2).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void extrapolate_kernel(const double* __restrict__ X1,
+                                                               const double* __restrict__ X2,
+                                                               double w,
+                                                               double* __restrict__ pred,
+                                                               int n, int F) {
+    const int bh = blockIdx.y;
+    const int a = blockIdx.x * kThreads + threadIdx.x;
+    const int m = 3 * n - 1, p = 3 * n - 1 + F;
+    if (a >= m) return;
+    const double x2 = X2[(size_t)bh * p + a], x1 = X1[(size_t)bh * p + a];
+    pred[(size_t)bh * m + a] = x2 + (x2 - x1) * w;
+}
+
+// ---------------------------------------------------------------------------
+// a5: per-row selection.  One workgroup per (head, query block i).
+//   sigma_j = n (c~[j-i] + d~[j]) in fp64, rounded to float: the ranking key.
+//   Non-forced blocks get the 64-bit key (order(sigma) << 32 | ~j), so one
+//   descending bitonic sort orders them by (sigma desc, j asc); forced blocks
+//   and padding get key 0 and sort last.
+//   TOPK keeps the first max(0, k - |forced|) sorted blocks; MASS keeps the
+//   shortest prefix whose positive key mass, added to the forced blocks'
+//   mass, reaches tau of the row total (fp64 prefix sums; at least one block).
+//   The kept set is compacted in ascending j.
+// ---------------------------------------------------------------------------
+__device__ inline uint32_t order_bits(float f) {
+    const uint32_t u = __float_as_uint(f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ inline float order_bits_to_float(uint32_t k) {
+    const uint32_t u = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
+    return __uint_as_float(u);
+}
+
+__global__ __launch_bounds__(kThreads) void select_kernel(
+    const double* __restrict__ pred, const int32_t* __restrict__ gate,
+    const int* __restrict__ row_lo, const int* __restrict__ row_hi, int mode, int topk,
+    double tau, int32_t* __restrict__ kv_idx, int32_t* __restrict__ kv_cnt, int n, int npad) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    uint64_t* keys = reinterpret_cast<uint64_t*>(smem);          // npad
+    double* scan = reinterpret_cast<double*>(keys + npad);        // npad
+    int* flag = reinterpret_cast<int*>(scan + npad);              // npad
+    __shared__ double red[kThreads];
+    __shared__ int ired[kThreads];
+    __shared__ int kk_shared;
+
+    const int row = blockIdx.x;
+    const int bh = row / n, i = row % n;
+    const double* c = pred + (size_t)bh * (3 * n - 1);
+    const double* d = c + (2 * n - 1);
+    const bool g = gate[bh] != 0;
+    const int flo = row_lo[i], fhi = row_hi[i];
+    const int nf = g ? (fhi - flo + 1) : 0;
+    const int n_free = n - nf;
+    const int t = threadIdx.x;
+
+    double forced_mass = 0.0;
+    for (int j = t; j < npad; j += kThreads) {
+        uint64_t key = 0;
+        int fl = 0;
+        if (j < n) {
+            const double s = static_cast<double>(n) * (c[j - i + n - 1] + d[j]);
+            const float kf = static_cast<float>(s);
+            if (g && j >= flo && j <= fhi) {
+                fl = 1;
+                forced_mass += fmax(static_cast<double>(kf), 0.0);
+            } else {
+                key = (static_cast<uint64_t>(order_bits(kf)) << 32) |
+                      static_cast<uint64_t>(0xFFFFFFFFu - static_cast<uint32_t>(j));
+            }
+        }
+        keys[j] = key;
+        flag[j] = fl;
+    }
+    __syncthreads();
+
+    // descending bitonic sort of keys[0, npad)
+    for (int kk = 2; kk <= npad; kk <<= 1) {
+        for (int jj = kk >> 1; jj > 0; jj >>= 1) {
+            for (int a = t; a < npad; a += kThreads) {
+                const int b = a ^ jj;
+                if (b > a) {
+                    const uint64_t ka = keys[a], kb = keys[b];
+                    const bool desc = (a & kk) == 0;
+                    if (desc ? (ka < kb) : (ka > kb)) {
+                        keys[a] = kb;
+                        keys[b] = ka;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    }
+
+    const int E = npad / kThreads;   // consecutive sorted positions per thread
+    int keep;
+    if (mode == 0) {
+        keep = min(n_free, max(0, topk - nf));
+    } else {
+        const double fm = block_sum(forced_mass, red);
+        // inclusive scan of the positive masses in sorted order
+        double run = 0.0;
+        for (int e = 0; e < E; ++e) {
+            const int pos = t * E + e;
+            const double v =
+                pos < n_free
+                    ? fmax(static_cast<double>(order_bits_to_float(
+                               static_cast<uint32_t>(keys[pos] >> 32))),
+                           0.0)
+                    : 0.0;
+            run += v;
+            scan[pos] = run;
+        }
+        red[t] = run;
+        __syncthreads();
+        if (t == 0) {
+            double off = 0.0;
+            for (int a = 0; a < kThreads; ++a) {
+                const double v = red[a];
+                red[a] = off;
+                off += v;
+            }
+        }
+        __syncthreads();
+        const double off = red[t];
+        for (int e = 0; e < E; ++e) scan[t * E + e] += off;
+        if (t == 0) kk_shared = n_free;
+        __syncthreads();
+        const double total = fm + scan[npad - 1];
+        const double target = tau * total;
+        const int kmin = nf > 0 ? 0 : 1;
+        for (int e = 0; e < E; ++e) {
+            const int cand = t * E + e;     // keep `cand` free blocks
+            if (cand < kmin || cand > n_free) continue;
+            const double cum = fm + (cand == 0 ? 0.0 : scan[cand - 1]);
+            if (cum >= target) atomicMin(&kk_shared, cand);
+        }
+        __syncthreads();
+        keep = kk_shared;
+    }
+    for (int a = t; a < keep; a += kThreads) {
+        const uint32_t j = 0xFFFFFFFFu - static_cast<uint32_t>(keys[a] & 0xFFFFFFFFull);
+        flag[j] = 1;
+    }
+    __syncthreads();
+
+    // compaction in ascending j
+    int cnt = 0;
+    for (int e = 0; e < E; ++e) cnt += flag[t * E + e];
+    ired[t] = cnt;
+    __syncthreads();
+    if (t == 0) {
+        int off = 0;
+        for (int a = 0; a < kThreads; ++a) {
+            const int v = ired[a];
+            ired[a] = off;
+            off += v;
+        }
+        kv_cnt[row] = off;
+    }
+    __syncthreads();
+    int pos = ired[t];
+    int32_t* out = kv_idx + (size_t)row * n;
+    for (int e = 0; e < E; ++e) {
+        const int j = t * E + e;
+        if (flag[j]) out[pos++] = j;
+    }
+}
+
+inline unsigned cdiv(long a, long b) { return static_cast<unsigned>((a + b - 1) / b); }
+
+}  // namespace
+
+hipError_t launch_pool(const uint16_t* q, const uint16_t* k, double* qbar, double* kbar,
+                       int BH, int L, int d, int bs, int n, hipStream_t s) {
+    const dim3 grid(n, BH, 2);
+    if (d == 128)
+        hipLaunchKernelGGL(pool_kernel<128>, grid, dim3(kThreads), 0, s, q, k, qbar, kbar, L, bs, n);
+    else
+        hipLaunchKernelGGL(pool_kernel<64>, grid, dim3(kThreads), 0, s, q, k, qbar, kbar, L, bs, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_block_mass(const double* qbar, const double* kbar, double* G, int BH,
+                             int L, int d, int bs, int n, double scale, hipStream_t s) {
+    const dim3 grid(cdiv(n, 64), cdiv(n, 64), BH);
+    if (d == 128)
+        hipLaunchKernelGGL(logits_kernel<128>, grid, dim3(kThreads), 0, s, qbar, kbar, G, n, scale);
+    else
+        hipLaunchKernelGGL(logits_kernel<64>, grid, dim3(kThreads), 0, s, qbar, kbar, G, n, scale);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(mass_softmax_kernel, dim3((unsigned)BH * n), dim3(kThreads), 0, s, G, L,
+                       bs, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_rhs(const double* G, const int* reg, double* r, int BH, int n, int F,
+                      hipStream_t s) {
+    const int p = 3 * n - 1 + F;
+    hipLaunchKernelGGL(rhs_kernel, dim3(cdiv(p, kThreads), BH), dim3(kThreads), 0, s, G, reg, r,
+                       n, F);
+    return hipGetLastError();
+}
+
+hipError_t launch_solve(const double* r, const int* reg, const double* Sinv, double* bU,
+                        double* u, double* X, int BH, int n, int F, hipStream_t s) {
+    const int q = n - 1 + F;
+    hipLaunchKernelGGL(solve_pre_kernel, dim3(BH), dim3(kThreads),
+                       (size_t)(2 * n - 1) * sizeof(double), s, r, reg, bU, n, F);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(solve_gemv_kernel, dim3(cdiv(q, kThreads), cdiv(BH, 4)), dim3(kThreads), 0,
+                       s, Sinv, bU, u, q, BH);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(solve_post_kernel, dim3(BH), dim3(kThreads), (size_t)q * sizeof(double), s,
+                       r, u, reg, X, n, F);
+    return hipGetLastError();
+}
+
+hipError_t launch_gate(const double* Xa, const double* Xb, int32_t* gate, int BH, int n,
+                       int F, double tau_e, hipStream_t s) {
+    hipLaunchKernelGGL(gate_kernel, dim3(cdiv(BH, 64)), dim3(64), 0, s, Xa, Xb, gate, BH, n, F,
+                       tau_e);
+    return hipGetLastError();
+}
+
+hipError_t launch_extrapolate(const double* X1, const double* X2, double w, double* pred,
+                              int BH, int n, int F, hipStream_t s) {
+    hipLaunchKernelGGL(extrapolate_kernel, dim3(cdiv(3 * n - 1, kThreads), BH), dim3(kThreads), 0,
+                       s, X1, X2, w, pred, n, F);
+    return hipGetLastError();
+}
+
+hipError_t launch_select(const double* pred, const int32_t* gate, const int* row_lo,
+                         const int* row_hi, int mode, int k, double tau, int32_t* kv_idx,
+                         int32_t* kv_cnt, int BH, int n, hipStream_t s) {
+    int npad = kThreads;
+    while (npad < n) npad <<= 1;
+    const size_t lds = (size_t)npad * (sizeof(uint64_t) + sizeof(double) + sizeof(int));
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_kernel),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)((size_t)kMaxBlocks * 20));
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    hipLaunchKernelGGL(select_kernel, dim3((unsigned)BH * n), dim3(kThreads), lds, s, pred, gate,
+                       row_lo, row_hi, mode, k, tau, kv_idx, kv_cnt, n, npad);
+    return hipGetLastError();
+}
+
+}  // namespace moddit

@@ -1,0 +1,89 @@
+"""The C-ABI library loads on a machine without a GPU, exports every entry
+point that include/moddit.h declares, and rejects bad arguments on the host
+before touching the device."""
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moddit.h")
+LIB = os.path.join(ROOT, "paper_2601_11641_amd", "libmoddit.so")
+
+
+@pytest.fixture(scope="module")
+def M():
+    if not os.path.exists(LIB):
+        from paper_2601_11641_amd import build_lib
+        build_lib.build()
+    import paper_2601_11641_amd as m
+    return m
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mod_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for core in ("mod_collect_stats", "mod_predict_block_mask", "mod_block_sparse_attn_fwd"):
+        assert core in names
+
+
+def test_library_exports_every_declared_symbol(M):
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r"\bT (mod_[a-z_]+)\b", out))
+    missing = [f for f in declared_functions() if f not in exported]
+    assert not missing, missing
+    assert set(M.EXPORTED) == set(declared_functions())
+
+
+def test_block_and_coefficient_counts(M):
+    s = M.make_shape(1, 24, 118800, 128, 128, 3600)
+    assert M.mod_num_blocks(s) == 929 and M.mod_num_coeffs(s) == 3 * 929 - 1 + 33
+    s = M.make_shape(1, 40, 75600, 128, 128, 3600)
+    assert M.mod_num_blocks(s) == 591 and M.mod_num_coeffs(s) == 3 * 591 - 1 + 21
+    assert M.mod_num_blocks(None) == 0
+    assert M.mod_num_coeffs(M.make_shape(1, 1, 100, 64, 64, 30)) == 0
+
+
+@pytest.mark.parametrize("shape,status", [
+    ((1, 2, 1024, 96, 64, 256), 2),      # d unsupported
+    ((1, 2, 1024, 64, 32, 256), 2),      # block unsupported
+    ((1, 2, 1024, 64, 64, 1000), 2),     # not whole frames
+    ((1, 2, 1024, 64, 64, 1024), 2),     # a single frame
+    ((0, 2, 1024, 64, 64, 256), 1),      # empty batch
+    ((1, 2, 1024, 64, 64, 0), 1),        # frame_tokens missing
+    ((1, 1, 128 * 4097, 64, 128, 128), 2),  # n above the limit
+])
+def test_create_rejects_bad_shapes_on_host(M, shape, status):
+    with pytest.raises(M.ModError) as e:
+        M.mod_stats_create(M.make_shape(*shape), M.make_params())
+    assert e.value.status == status
+    assert M.mod_last_error()
+
+
+def test_create_rejects_bad_params(M):
+    with pytest.raises(M.ModError) as e:
+        M.mod_stats_create(M.make_shape(1, 2, 1024, 64, 64, 256), M.make_params(anchor_rule=3))
+    assert e.value.status == M.MOD_ERR_INVALID_ARG
+
+
+def test_attention_rejects_null_pointers_on_host(M):
+    lib = M.raw_lib()
+    s = M.make_shape(1, 2, 1024, 64, 64, 256)
+    import ctypes
+    st = lib.mod_block_sparse_attn_fwd(ctypes.byref(s), None, None, None, None, None, 0.0, None,
+                                       None, None, 0, None)
+    assert st == M.MOD_ERR_INVALID_ARG
+    st = lib.mod_block_sparse_attn_fwd(None, 1, 1, 1, 1, 1, 0.0, 1, None, None, 0, None)
+    assert st == M.MOD_ERR_INVALID_ARG
+    assert M.mod_status_string(st) == "MOD_ERR_INVALID_ARG"
+
+
+def test_workspace_size(M):
+    assert M.mod_attn_workspace_bytes(M.make_shape(1, 24, 118800, 128, 128, 3600)) >= 0

@@ -1,0 +1,240 @@
+"""GPU parity of the whole hot path against the CPU oracle, through the C ABI.
+
+Sizes the oracle finishes in seconds: the tiny and small layers of the
+workload set, plus ragged shapes (short tail block, frames straddling
+blocks, d/block combinations) chosen to span several tiles and a ragged
+tail.  The 720p layers are covered by test_gpu_720p.py.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from parity import (GAP, LSE_ABS, MAX_ABS, MEAN_ABS, attention_errors, bf16_tensor, bf16_to_f64,
+                    compare_lists, gpu_lists)
+
+import paper_2601_11641_amd as M
+
+torch = pytest.importorskip("torch")
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+
+def _cfg(base, **kw):
+    c = W.CONFIGS[base]
+    d = dict(name=c.name, B=c.B, H=c.H, d=c.d, frames=c.frames, hs=c.hs, ws=c.ws,
+             block=c.block, seed=c.seed)
+    d.update(kw)
+    return W.LayerConfig(**d)
+
+
+RAGGED = {
+    # 5 frames of 9x25 = 225 tokens, block 128: n = 9, tail 101, frames straddle blocks
+    "ragged128": _cfg("small", name="ragged128", B=2, H=3, frames=5, hs=9, ws=25, seed=5),
+    # d 128 with block 64: 6 frames of 10x20 = 200 tokens, n = 19, tail 48
+    "d128b64": _cfg("small", name="d128b64", B=1, H=3, frames=6, hs=10, ws=20, block=64, seed=6),
+    # d 64 with block 128: 7 frames of 12x15 = 180 tokens, n = 10, tail 108
+    "d64b128": _cfg("tiny", name="d64b128", B=1, H=3, frames=7, hs=12, ws=15, block=128, seed=7),
+    # d 64, block 64, long: 3 frames of 24x40 = 960, n = 45
+    "d64b64": _cfg("tiny", name="d64b64", B=1, H=2, frames=3, hs=24, ws=40, block=64, seed=8),
+}
+
+
+def _inputs(cfg):
+    q, k, v = W.generate(cfg)
+    return (q, k, v), tuple(bf16_tensor(x) for x in (q, k, v))
+
+
+def _run_predictor(cfg, dev, host, warm, step, budget, params):
+    qd, kd, _ = dev
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    st = M.Stats(shape, M.make_params(**params))
+    for t in warm:
+        M.mod_collect_stats(st.handle, qd, kd, t)
+    n = st.n
+    kv_idx = torch.full((cfg.B, cfg.H, n, n), -1, dtype=torch.int32, device="cuda")
+    kv_cnt = torch.zeros((cfg.B, cfg.H, n), dtype=torch.int32, device="cuda")
+    mode, val = budget
+    gb = M.make_budget(mode, density=val) if mode == "topk" else M.make_budget(mode, mass=val)
+    M.mod_predict_block_mask(st.handle, qd, kd, step, gb, kv_idx, kv_cnt)
+    torch.cuda.synchronize()
+
+    qf, kf = W.bf16_bits_to_f64(host[0]), W.bf16_bits_to_f64(host[1])
+    P = O.Predictor(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens, **params)
+    for t in warm:
+        P.collect(qf, kf, t)
+    mode, val = budget
+    ob = O.Budget(mode, density=val if mode == "topk" else 1.0, mass=val if mode == "mass" else 1.0)
+    sel = P.predict(qf, kf, step, ob)
+    return st, kv_idx, kv_cnt, P, sel, qf, kf
+
+
+def _check_predictor(cfg, st, kv_idx, kv_cnt, P, sel, qf, kf, budget, step):
+    B, H, n = cfg.B, cfg.H, st.n
+    # a1 / a2 / a3 intermediate parity (fp64 on both sides)
+    qb, kb = M.mod_stats_get_pooled(st.handle, B, H, n, cfg.d)
+    np.testing.assert_allclose(qb, O.pool(qf, cfg.block), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(kb, O.pool(kf, cfg.block), rtol=1e-12, atol=1e-13)
+    G = M.mod_stats_get_block_mass(st.handle, B, H, n)
+    np.testing.assert_allclose(G, P.pooled_mass(qf, kf), rtol=1e-10, atol=1e-15)
+    X, t2 = M.mod_stats_get_anchor(st.handle, 0, B, H, st.p)
+    Xo = P.anchors[-1][1]
+    assert t2 == P.anchors[-1][0]
+    assert np.abs(X - Xo).max() <= 1e-9 * max(1.0, np.abs(Xo).max())
+    gate = M.mod_stats_get_gate(st.handle, B, H)
+    assert (gate.astype(bool) == P.gates).all()
+    pred = M.mod_stats_get_prediction(st.handle, B, H, n)
+    po = P.prediction(step)
+    for b in range(B):
+        for h in range(H):
+            ct, dt_ = po[b][h]
+            ref = np.concatenate([ct, dt_])
+            assert np.abs(pred[b, h] - ref).max() <= 1e-9 * max(1.0, np.abs(ref).max())
+    # a5 list parity
+    rows = gpu_lists(kv_idx, kv_cnt)
+    mode, val = budget
+    k = O.topk_count(val, n) if mode == "topk" else 0
+    tau = val if mode == "mass" else 1.0
+    total = exact = excused = 0
+    for b in range(B):
+        for h in range(H):
+            ct, dt_ = po[b][h]
+            sig = O.scores(ct, dt_, n)
+            forced = O.forced_mask(n, P.regions, bool(P.gates[b, h]))
+            nr, ne, nx, bad = compare_lists(rows[b][h], sel[b][h], sig, forced, mode, k, tau)
+            assert not bad, f"head ({b},{h}) rows {bad[:10]} differ beyond the gap rule"
+            total, exact, excused = total + nr, exact + ne, excused + nx
+    assert excused <= max(2, 0.02 * total), (excused, total)
+    return rows
+
+
+def _check_attention(cfg, dev, host, rows, rtol_rows=None):
+    qd, kd, vd = dev
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    o = torch.empty_like(qd)
+    lse = torch.empty((cfg.B, cfg.H, cfg.L), dtype=torch.float32, device="cuda")
+    n = M.mod_num_blocks(shape)
+    idx = torch.zeros((cfg.B, cfg.H, n, n), dtype=torch.int32)
+    cnt = torch.zeros((cfg.B, cfg.H, n), dtype=torch.int32)
+    for b in range(cfg.B):
+        for h in range(cfg.H):
+            for i, js in enumerate(rows[b][h]):
+                cnt[b, h, i] = len(js)
+                idx[b, h, i, :len(js)] = torch.tensor(js, dtype=torch.int32)
+    M.mod_block_sparse_attn_fwd(shape, qd, kd, vd, idx.cuda(), cnt.cuda(), 0.0, o, lse)
+    torch.cuda.synchronize()
+    og = bf16_to_f64(o)
+    lg = lse.cpu().numpy().astype(np.float64)
+    scale = 1.0 / math.sqrt(cfg.d)
+    worst = (0.0, 0.0)
+    for b in range(cfg.B):
+        for h in range(cfg.H):
+            qf, kf, vf = (W.bf16_bits_to_f64(x[b, h]) for x in host)
+            Oo, Lo = O.attention(qf, kf, vf, rows[b][h], cfg.block, scale)
+            mx, mean = attention_errors(og[b, h], Oo)
+            assert mx <= MAX_ABS and mean <= MEAN_ABS, (b, h, mx, mean)
+            fin = np.isfinite(Lo)
+            assert (np.isneginf(lg[b, h][~fin])).all()
+            assert np.abs(lg[b, h][fin] - Lo[fin]).max() <= LSE_ABS
+            worst = (max(worst[0], mx), max(worst[1], mean))
+    return worst
+
+
+@pytest.mark.parametrize("budget", [("topk", 0.3), ("mass", 0.8)])
+def test_tiny_predictor_and_attention(budget):
+    cfg = W.CONFIGS["tiny"]
+    host, dev = _inputs(cfg)
+    params = dict(warmup_m=1, delta_t=0)
+    st, kv_idx, kv_cnt, P, sel, qf, kf = _run_predictor(cfg, dev, host, [1], 2, budget, params)
+    rows = _check_predictor(cfg, st, kv_idx, kv_cnt, P, sel, qf, kf, budget, 2)
+    _check_attention(cfg, dev, host, rows)
+    st.close()
+
+
+@pytest.mark.parametrize("density", [1.0, 0.5, 0.25])
+def test_small_topk_densities(density):
+    cfg = W.CONFIGS["small"]
+    host, dev = _inputs(cfg)
+    params = dict(warmup_m=5, delta_t=10)
+    budget = ("topk", density)
+    st, kv_idx, kv_cnt, P, sel, qf, kf = _run_predictor(cfg, dev, host, [4, 5], 6, budget, params)
+    rows = _check_predictor(cfg, st, kv_idx, kv_cnt, P, sel, qf, kf, budget, 6)
+    if density == 1.0:
+        assert all(r == list(range(st.n)) for hh in rows[0] for r in hh)
+    _check_attention(cfg, dev, host, rows)
+    st.close()
+
+
+def test_small_full_mask_equals_dense_attention():
+    """Density 1 lists give textbook dense softmax attention."""
+    cfg = W.CONFIGS["small"]
+    host, dev = _inputs(cfg)
+    n = cfg.n
+    rows = [[[list(range(n)) for _ in range(n)] for _ in range(cfg.H)]]
+    mx, mean = _check_attention(cfg, dev, host, rows)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS
+
+
+def test_small_mass_mode():
+    cfg = W.CONFIGS["small"]
+    host, dev = _inputs(cfg)
+    params = dict(warmup_m=5, delta_t=10, tau_e=0.0)
+    budget = ("mass", 0.85)
+    st, kv_idx, kv_cnt, P, sel, qf, kf = _run_predictor(cfg, dev, host, [4, 5], 7, budget, params)
+    rows = _check_predictor(cfg, st, kv_idx, kv_cnt, P, sel, qf, kf, budget, 7)
+    _check_attention(cfg, dev, host, rows)
+    st.close()
+
+
+@pytest.mark.parametrize("name", sorted(RAGGED))
+@pytest.mark.parametrize("budget", [("topk", 0.4), ("mass", 0.7)])
+def test_ragged_shapes(name, budget):
+    cfg = RAGGED[name]
+    host, dev = _inputs(cfg)
+    params = dict(warmup_m=2, delta_t=0)
+    st, kv_idx, kv_cnt, P, sel, qf, kf = _run_predictor(cfg, dev, host, [1, 2], 4, budget, params)
+    rows = _check_predictor(cfg, st, kv_idx, kv_cnt, P, sel, qf, kf, budget, 4)
+    _check_attention(cfg, dev, host, rows)
+    st.close()
+
+
+def test_attention_empty_and_single_rows():
+    """Rows with no kept block give O = 0 and lse = -inf; single-block rows
+    match the oracle."""
+    cfg = RAGGED["ragged128"]
+    host, dev = _inputs(cfg)
+    n = cfg.n
+    rng = np.random.default_rng(0)
+    rows = [[[([] if i % 3 == 0 else [int(rng.integers(n))]) for i in range(n)]
+             for _ in range(cfg.H)] for _ in range(cfg.B)]
+    _check_attention(cfg, dev, host, rows)
+
+
+def test_state_errors_on_device():
+    cfg = W.CONFIGS["tiny"]
+    _, dev = _inputs(cfg)
+    qd, kd, _ = dev
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    st = M.Stats(shape, M.make_params(warmup_m=2, delta_t=3))
+    n = st.n
+    idx = torch.empty((cfg.B, cfg.H, n, n), dtype=torch.int32, device="cuda")
+    cnt = torch.empty((cfg.B, cfg.H, n), dtype=torch.int32, device="cuda")
+    with pytest.raises(M.ModError) as e:
+        M.mod_predict_block_mask(st.handle, qd, kd, 3, M.make_budget("topk", 0.5), idx, cnt)
+    assert e.value.status == M.MOD_ERR_BAD_STATE
+    M.mod_collect_stats(st.handle, qd, kd, 1)
+    with pytest.raises(M.ModError) as e:
+        M.mod_collect_stats(st.handle, qd, kd, 1)
+    assert e.value.status == M.MOD_ERR_BAD_STATE
+    with pytest.raises(M.ModError) as e:
+        M.mod_predict_block_mask(st.handle, qd, kd, 3, M.make_budget("topk", 0.0), idx, cnt)
+    assert e.value.status == M.MOD_ERR_INVALID_ARG
+    with pytest.raises(M.ModError) as e:   # step 5 = m + dt re-anchors: q, k needed
+        M.mod_predict_block_mask(st.handle, None, None, 5, M.make_budget("topk", 0.5), idx, cnt)
+    assert e.value.status == M.MOD_ERR_INVALID_ARG
+    M.mod_predict_block_mask(st.handle, None, None, 3, M.make_budget("topk", 0.5), idx, cnt)
+    torch.cuda.synchronize()
+    assert int(cnt.min()) >= O.topk_count(0.5, n)
+    st.close()
