@@ -1,0 +1,142 @@
+"""GPU parity at the full 720p layer sizes, in the launch configuration the
+benchmark times (whole layer on the device), checked on sampled outputs the
+oracle computes head by head: every query block of a few heads of each head
+type for the selection, and sampled query blocks (including the short tail
+block) for the attention."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle as O
+import paper_2601_11641_amd as M
+import workloads as W
+from parity import (LSE_ABS, MAX_ABS, MEAN_ABS, attention_errors, bf16_tensor, bf16_to_f64,
+                    compare_lists, gpu_lists)
+
+torch = pytest.importorskip("torch")
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+WARM = 5
+
+
+@pytest.fixture(scope="module", params=["hunyuan", "wan"])
+def layer(request):
+    cfg = W.CONFIGS[request.param]
+    host = W.generate(cfg)
+    dev = tuple(bf16_tensor(x) for x in host)
+    return cfg, host, dev
+
+
+def _sample_heads(cfg):
+    """Two heads of each type (the types are seeded 1/3 each)."""
+    types = W.head_types(cfg)
+    heads = []
+    for t in (W.HEAD_TEMPORAL, W.HEAD_SPATIAL, W.HEAD_GLOBAL):
+        heads += [int(h) for h in np.flatnonzero(types == t)[:2]]
+    return sorted(heads)
+
+
+def _gpu_predict(cfg, dev, budget):
+    qd, kd, _ = dev
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    st = M.Stats(shape, M.make_params(warmup_m=WARM, delta_t=1))
+    M.mod_collect_stats(st.handle, qd, kd, WARM - 1)
+    M.mod_collect_stats(st.handle, qd, kd, WARM)
+    n = st.n
+    idx = torch.empty((cfg.B, cfg.H, n, n), dtype=torch.int32, device="cuda")
+    cnt = torch.empty((cfg.B, cfg.H, n), dtype=torch.int32, device="cuda")
+    mode, val = budget
+    gb = M.make_budget(mode, density=val) if mode == "topk" else M.make_budget(mode, mass=val)
+    M.mod_predict_block_mask(st.handle, qd, kd, WARM + 1, gb, idx, cnt)
+    torch.cuda.synchronize()
+    return st, idx, cnt
+
+
+def _check_heads(cfg, host, st, idx, cnt, budget, heads):
+    sub = W.generate_heads(cfg, heads=heads)
+    for a, b in zip(sub, host):
+        assert np.array_equal(a[0], b[0, heads])
+    qf, kf = W.bf16_bits_to_f64(sub[0]), W.bf16_bits_to_f64(sub[1])
+    P = O.Predictor(1, len(heads), cfg.L, cfg.d, cfg.block, cfg.frame_tokens, warmup_m=WARM,
+                    delta_t=1)
+    P.collect(qf, kf, WARM - 1)
+    P.collect(qf, kf, WARM)
+    mode, val = budget
+    sel = P.predict(qf, kf, WARM + 1, O.Budget(mode, density=val if mode == "topk" else 1.0,
+                                               mass=val if mode == "mass" else 1.0))
+    n = st.n
+    X, _ = M.mod_stats_get_anchor(st.handle, 0, cfg.B, cfg.H, st.p)
+    Xo = P.anchors[-1][1]
+    gate = M.mod_stats_get_gate(st.handle, cfg.B, cfg.H)
+    rows = gpu_lists(idx, cnt)
+    k = O.topk_count(val, n) if mode == "topk" else 0
+    tau = val if mode == "mass" else 1.0
+    total = excused = 0
+    for hi, h in enumerate(heads):
+        assert np.abs(X[0, h] - Xo[0, hi]).max() <= 1e-9 * max(1.0, np.abs(Xo[0, hi]).max())
+        assert bool(gate[0, h]) == bool(P.gates[0, hi])
+        ct, dt_ = P.prediction(WARM + 1)[0][hi]
+        sig = O.scores(ct, dt_, n)
+        forced = O.forced_mask(n, P.regions, bool(P.gates[0, hi]))
+        nr, _, nx, bad = compare_lists(rows[0][h], sel[0][hi], sig, forced, mode, k, tau)
+        assert not bad, f"head {h}: rows {bad[:10]} differ beyond the gap rule"
+        total, excused = total + nr, excused + nx
+    assert excused <= max(2, 0.01 * total), (excused, total)
+    return rows
+
+
+def _check_attention_rows(cfg, host, dev, idx, cnt, heads, nrows=5):
+    qd, kd, vd = dev
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    o = torch.empty_like(qd)
+    lse = torch.empty((cfg.B, cfg.H, cfg.L), dtype=torch.float32, device="cuda")
+    M.mod_block_sparse_attn_fwd(shape, qd, kd, vd, idx, cnt, 0.0, o, lse)
+    torch.cuda.synchronize()
+    rows = gpu_lists(idx, cnt)
+    n = cfg.n
+    rng = np.random.default_rng(42)
+    for h in heads:
+        sample = sorted(set(rng.choice(n - 1, size=nrows - 1, replace=False).tolist()) | {n - 1})
+        qf, kf, vf = (W.bf16_bits_to_f64(x[0, h]) for x in host)
+        Oo, Lo = O.attention(qf, kf, vf, rows[0][h], cfg.block, 1.0 / math.sqrt(cfg.d), rows=sample)
+        og = bf16_to_f64(o[0, h])
+        lg = lse[0, h].cpu().numpy().astype(np.float64)
+        for i in sample:
+            sl = slice(i * cfg.block, min(cfg.L, (i + 1) * cfg.block))
+            mx, mean = attention_errors(og[sl], Oo[sl])
+            assert mx <= MAX_ABS and mean <= MEAN_ABS, (h, i, mx, mean)
+            assert np.abs(lg[sl] - Lo[sl]).max() <= LSE_ABS
+
+
+def test_720p_mass_budget(layer):
+    """The benchmark's budget (cumulative mass 0.75) on the whole layer."""
+    cfg, host, dev = layer
+    budget = ("mass", 0.75)
+    st, idx, cnt = _gpu_predict(cfg, dev, budget)
+    heads = _sample_heads(cfg)
+    _check_heads(cfg, host, st, idx, cnt, budget, heads)
+    _check_attention_rows(cfg, host, dev, idx, cnt, heads)
+    st.close()
+
+
+@pytest.mark.parametrize("density", [0.5, 0.1, 0.05])
+def test_720p_topk_densities(layer, density):
+    cfg, host, dev = layer
+    budget = ("topk", density)
+    st, idx, cnt = _gpu_predict(cfg, dev, budget)
+    heads = _sample_heads(cfg)[::2]
+    _check_heads(cfg, host, st, idx, cnt, budget, heads)
+    _check_attention_rows(cfg, host, dev, idx, cnt, heads, nrows=3)
+    st.close()
+
+
+def test_720p_full_mask_is_dense_attention(layer):
+    """Full lists at 720p: sampled query blocks equal dense softmax attention."""
+    cfg, host, dev = layer
+    n = cfg.n
+    idx = torch.arange(n, dtype=torch.int32, device="cuda").repeat(cfg.B * cfg.H * n).reshape(
+        cfg.B, cfg.H, n, n)
+    cnt = torch.full((cfg.B, cfg.H, n), n, dtype=torch.int32, device="cuda")
+    _check_attention_rows(cfg, host, dev, idx, cnt, [0, cfg.H - 1], nrows=3)

@@ -238,3 +238,51 @@ def test_state_errors_on_device():
     torch.cuda.synchronize()
     assert int(cnt.min()) >= O.topk_count(0.5, n)
     st.close()
+
+
+@pytest.mark.parametrize("rule", [0, 1])
+def test_schedule_with_drift(rule):
+    """Denoising schedule with smoothly drifting Q/K (two seeded draws mixed
+    by angle): warm-up anchors at steps 4 and 5, then sparse steps 6..30 with
+    re-anchoring every 10 steps; the masks of every step match the oracle."""
+    base = W.CONFIGS["small"]
+    cfg = _cfg("small", H=3)
+    T = 30
+    a = W.generate(cfg)
+    b = W.generate_heads(cfg, seed=base.seed + 1000)
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    params = dict(warmup_m=5, delta_t=10, anchor_rule=rule)
+    st = M.Stats(shape, M.make_params(**params))
+    P = O.Predictor(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens, **params)
+    n = st.n
+    idx = torch.empty((cfg.B, cfg.H, n, n), dtype=torch.int32, device="cuda")
+    cnt = torch.empty((cfg.B, cfg.H, n), dtype=torch.int32, device="cuda")
+    budget = ("topk", 0.3)
+    k = O.topk_count(0.3, n)
+    anchors = []
+    for t in range(4, T + 1):
+        qb = W.drift_mix(a[0], b[0], t, T)
+        kb = W.drift_mix(a[1], b[1], t, T)
+        qd, kd = bf16_tensor(qb), bf16_tensor(kb)
+        qf, kf = W.bf16_bits_to_f64(qb), W.bf16_bits_to_f64(kb)
+        if t <= 5:
+            M.mod_collect_stats(st.handle, qd, kd, t)
+            P.collect(qf, kf, t)
+            continue
+        M.mod_predict_block_mask(st.handle, qd, kd, t, M.make_budget("topk", density=0.3), idx, cnt)
+        sel = P.predict(qf, kf, t, O.Budget("topk", density=0.3))
+        if P.is_anchor_step(t):
+            anchors.append(t)
+        torch.cuda.synchronize()
+        rows = gpu_lists(idx, cnt)
+        pred = P.prediction(t)
+        for h in range(cfg.H):
+            sig = O.scores(*pred[0][h], n)
+            forced = O.forced_mask(n, P.regions, bool(P.gates[0, h]))
+            _, _, _, bad = compare_lists(rows[0][h], sel[0][h], sig, forced, "topk", k)
+            assert not bad, (t, h, bad[:5])
+    assert anchors == ([15, 25] if rule == 0 else [10, 20, 30])
+    _, t2 = M.mod_stats_get_anchor(st.handle, 0, cfg.B, cfg.H, st.p)
+    _, t1 = M.mod_stats_get_anchor(st.handle, 1, cfg.B, cfg.H, st.p)
+    assert (t1, t2) == tuple(anchors[-2:])
+    st.close()

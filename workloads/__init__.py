@@ -26,7 +26,9 @@ Every random draw is made with numpy's PCG64 from a seed sequence keyed by
 """
 from __future__ import annotations
 
+import concurrent.futures
 import math
+import os
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -153,37 +155,53 @@ def head_bandwidths(cfg: LayerConfig, b: int, h: int, htype: int):
     return wt * ft, wsp * fs
 
 
-def positional_features(cfg: LayerConfig, omega_t: float, omega_s: float,
-                        kappa: float = KAPPA) -> np.ndarray:
-    """phi [L, d] float32 for the given frame/spatial base frequencies
-    (frame-first token order)."""
+def axis_features(cfg: LayerConfig, omega_t: float, omega_s: float, kappa: float = KAPPA):
+    """Per-axis positional features (frame [F, d/4], row [Hs, 3d/8], column
+    [Ws, 3d/8]) for the given base frequencies; the feature of token (f, y, x)
+    is their concatenation, which has RMS ``kappa`` over its d entries."""
     d = cfg.d
     dt = d // 4
     ds = (d - dt) // 2
-    wt, wsp = omega_t, omega_s
-    ft = _axis_features(np.arange(cfg.frames), dt, wt)          # [F, dt]
-    fy = _axis_features(np.arange(cfg.hs), ds, wsp)             # [Hs, ds]
-    fx = _axis_features(np.arange(cfg.ws), ds, wsp)             # [Ws, ds]
-    phi = np.empty((cfg.frames, cfg.hs, cfg.ws, d), dtype=np.float64)
+    # every sin/cos pair has squared norm 1, so sqrt(2)*kappa gives RMS kappa
+    a = math.sqrt(2.0) * kappa
+    return (a * _axis_features(np.arange(cfg.frames), dt, omega_t),
+            a * _axis_features(np.arange(cfg.hs), ds, omega_s),
+            a * _axis_features(np.arange(cfg.ws), ds, omega_s))
+
+
+def positional_features(cfg: LayerConfig, omega_t: float, omega_s: float,
+                        kappa: float = KAPPA) -> np.ndarray:
+    """phi [L, d] float32 in frame-first token order."""
+    ft, fy, fx = axis_features(cfg, omega_t, omega_s, kappa)
+    dt, ds = ft.shape[1], fy.shape[1]
+    phi = np.empty((cfg.frames, cfg.hs, cfg.ws, cfg.d), dtype=np.float64)
     phi[..., :dt] = ft[:, None, None, :]
     phi[..., dt:dt + ds] = fy[None, :, None, :]
     phi[..., dt + ds:] = fx[None, None, :, :]
-    # every sin/cos pair has squared norm 1, so sqrt(2)*kappa gives RMS kappa
-    phi *= math.sqrt(2.0) * kappa
-    return phi.reshape(cfg.L, d).astype(np.float32)
+    return phi.reshape(cfg.L, cfg.d).astype(np.float32)
 
 
 def _head_rng(seed: int, b: int, h: int, tag: int = 0) -> np.random.Generator:
     return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, b, h, tag])))
 
 
-def _draw_head(cfg: LayerConfig, b: int, h: int, htype: int, phi: np.ndarray,
-               seed: int | None = None):
-    """float32 Q, K, V [L, d] of one head before bf16 rounding."""
+def _draw_head(cfg: LayerConfig, b: int, h: int, htype: int, axes, seed: int | None = None):
+    """float32 Q, K, V [L, d] of one head before bf16 rounding.  ``axes``:
+    the per-axis features; phi R is formed as the sum of the three axis
+    blocks times the matching rows of R (same product, fewer flops)."""
     rng = _head_rng(cfg.seed if seed is None else seed, b, h)
     d, L = cfg.d, cfg.L
     R, _ = np.linalg.qr(rng.standard_normal((d, d)))
-    base = (phi @ R.astype(np.float32)) * np.float32(_FEATURE_WEIGHT)
+    ft, fy, fx = axes
+    dt, ds = ft.shape[1], fy.shape[1]
+    w = _FEATURE_WEIGHT
+    at = (w * ft @ R[:dt]).astype(np.float32)
+    ay = (w * fy @ R[dt:dt + ds]).astype(np.float32)
+    ax = (w * fx @ R[dt + ds:]).astype(np.float32)
+    base = np.empty((cfg.frames, cfg.hs, cfg.ws, d), dtype=np.float32)
+    np.add(at[:, None, None, :], ay[None, :, None, :], out=base)
+    base += ax[None, None, :, :]
+    base = base.reshape(L, d)
     q = base + np.float32(_NOISE_WEIGHT) * rng.standard_normal((L, d), dtype=np.float32)
     k = base + np.float32(_NOISE_WEIGHT) * rng.standard_normal((L, d), dtype=np.float32)
     v = rng.standard_normal((L, d), dtype=np.float32)
@@ -218,14 +236,25 @@ def generate_heads(cfg: LayerConfig, heads=None, batches=None, seed: int | None 
     types = head_types(cfg)
     shape = (len(batches), len(heads), cfg.L, cfg.d)
     out = [np.empty(shape, dtype=np.uint16) for _ in range(3)]
-    for bi, b in enumerate(batches):
-        for hi, h in enumerate(heads):
-            t = int(types[h])
-            phi = positional_features(cfg, *head_bandwidths(cfg, b, h, t), kappa=kappa)
-            q, k, v = _draw_head(cfg, b, h, t, phi, seed)
-            out[0][bi, hi] = to_bf16_bits(q)
-            out[1][bi, hi] = to_bf16_bits(k)
-            out[2][bi, hi] = to_bf16_bits(v)
+
+    def one(bi, b, hi, h):
+        t = int(types[h])
+        axes = axis_features(cfg, *head_bandwidths(cfg, b, h, t), kappa=kappa)
+        q, k, v = _draw_head(cfg, b, h, t, axes, seed)
+        out[0][bi, hi] = to_bf16_bits(q)
+        out[1][bi, hi] = to_bf16_bits(k)
+        out[2][bi, hi] = to_bf16_bits(v)
+
+    jobs = [(bi, b, hi, h) for bi, b in enumerate(batches) for hi, h in enumerate(heads)]
+    # heads draw from their own generators, so the result does not depend on
+    # the number of worker threads
+    workers = max(1, min(len(jobs), os.cpu_count() or 1, 16))
+    if workers == 1:
+        for j in jobs:
+            one(*j)
+    else:
+        with concurrent.futures.ThreadPoolExecutor(max_workers=workers) as ex:
+            list(ex.map(lambda j: one(*j), jobs))
     return out[0], out[1], out[2]
 
 
