@@ -1,175 +1,318 @@
 // Block-sparse attention forward for gfx950 (Eq. 1 with a block mask).
 //
-// One workgroup per (head, query block i); BS/32 waves, each owning 32 query
-// rows.  For every kept key block j of the row's list the K tile and the
-// transposed V tile are staged in LDS, and each wave computes
+// One workgroup per (head, query block i of BS rows).  The workgroup has
+// 2 * BS/64 waves: wave w owns 64 query rows (q-half w % (BS/64)) and one
+// half of every key/value tile (kv-half w / (BS/64)).  Each wave runs its own
+// online softmax over its kv halves; the two partial results of a q-half are
+// merged through LDS at the end.  Splitting the tile this way halves the LDS
+// bytes read per MFMA flop compared with 32-row waves over whole tiles.
 //
-//   S^T (BS x 32)  = K_j (BS x D) . Q^T (D x 32)      v_mfma_f32_32x32x16_bf16
-//   online softmax over the kv dimension in fp32 registers
-//   O^T (D x 32)  += V_j^T (D x BS) . P^T (BS x 32)   v_mfma_f32_32x32x16_bf16
-//
-// Computing the transposed products puts one query row in the column of
-// every lane, so the row max and the rescale of the accumulator are
-// per-lane scalars (one cross-half exchange per tile), and the fp32
-// probabilities of S^T feed the next MFMA as its B operand without moving
-// between lanes: the K rows are loaded in a permuted order that makes the
-// accumulator rows of a lane exactly the 8 consecutive kv positions the
-// B operand of the PV product expects.
+// Per kept key block j of the row's list:
+//   * the K and V tiles (BS x D bf16, row-major, 16-byte chunks XOR-swizzled
+//     per row) are brought into LDS with global_load_lds_dwordx4 one tile
+//     ahead (double buffer), so the copy of tile t+1 overlaps compute on t;
+//   * S^T (kv x q) = K . Q^T with v_mfma_f32_32x32x16_bf16: a lane owns one
+//     query column, so the row max and the rescale are per-lane scalars;
+//   * P = exp2(S * scale*log2e - m) in fp32, rounded to bf16 as the B operand
+//     of the next product without moving between lanes;
+//   * O^T (d x q) += V^T . P^T, the V^T operand read from the row-major V
+//     tile with ds_read_b64_tr_b16 (transposing LDS reads).
+// The running max is only moved when a tile's max exceeds it by more than
+// 2^8 in probability units, so most tiles skip the accumulator rescale.
 #include "moddit_internal.h"
 
 namespace moddit {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
+typedef short s16x4 __attribute__((__vector_size__(4 * sizeof(short))));
+typedef short s16x8 __attribute__((__vector_size__(8 * sizeof(short))));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
+typedef __attribute__((address_space(1))) void gbl_void_t;
 
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kRescaleLog2 = 8.0f;   // lazy-rescale threshold (log2 units)
 
-__device__ inline bf16x8 load_bf16x8(const uint16_t* p) {
-    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
+// XOR pattern applied to the 16-byte chunk index of a tile row.  The MFMA
+// operand loads read one chunk column of 8 consecutive rows per LDS cycle and
+// the transposing loads read two adjacent chunks of 4 consecutive rows; with
+// this pattern both land on distinct banks.
+template <int D>
+__device__ __forceinline__ int swz(int row) {
+    if constexpr (D == 128)
+        return (2 * row + ((row >> 3) & 1)) & 15;
+    else
+        return (2 * row + ((row >> 2) & 1)) & 7;
 }
 
+// Issue this wave's share of the 1-KB direct-to-LDS copies of one BS x D
+// tile.  Copy `ins` fills LDS bytes [ins*1024, +1024): lane l writes the
+// 16-byte chunk at ins*1024 + 16*l, i.e. row ins*RPI + l/LPR, physical
+// chunk l % LPR, which holds logical chunk (l % LPR) ^ swz(row).  The
+// per-lane part of the source offset only depends on ins mod 4 (D = 128) or
+// not at all (D = 64); it is precomputed in voff.  Rows past the end of the
+// sequence (short tail tile) re-read the last valid row: their scores are
+// masked and their probabilities are zero.
+template <int D, int BS, int NW>
+struct TileCopy {
+    static constexpr int ROWB = 2 * D;            // bytes per row
+    static constexpr int LPR = ROWB / 16;         // lanes per row
+    static constexpr int RPI = 64 / LPR;          // rows per 1-KB copy
+    static constexpr int IPW = BS * ROWB / 1024 / NW;
+    static constexpr int NV = D == 128 ? 4 : 1;
+    int voff[NV];                                  // element offsets, lane part
+
+    __device__ __forceinline__ TileCopy(int w, int lane) {
+#pragma unroll
+        for (int a = 0; a < NV; ++a) {
+            const int row = a * RPI + lane / LPR;  // row mod 16 (D=128) / mod 8 (D=64)
+            voff[a] = (lane / LPR) * D + (((lane % LPR) ^ swz<D>(row)) << 3);
+        }
+        (void)w;
+    }
+
+    __device__ __forceinline__ void issue(const uint16_t* __restrict__ g, int k0, int kvalid,
+                                          char* tile, int w, int lane) const {
+        if (kvalid == BS) {
+            const uint16_t* gt = g + (size_t)k0 * D;
+#pragma unroll
+            for (int ii = 0; ii < IPW; ++ii) {
+                const int ins = w * IPW + ii;
+                const uint16_t* src = gt + ins * RPI * D + voff[ii % NV];
+                __builtin_amdgcn_global_load_lds((gbl_void_t*)src, (lds_void_t*)(tile + ins * 1024),
+                                                 16, 0, 0);
+            }
+        } else {
+#pragma unroll
+            for (int ii = 0; ii < IPW; ++ii) {
+                const int ins = w * IPW + ii;
+                const int row = ins * RPI + lane / LPR;
+                const int chunk = (lane % LPR) ^ swz<D>(row);
+                const uint16_t* src = g + (size_t)(k0 + min(row, kvalid - 1)) * D + chunk * 8;
+                __builtin_amdgcn_global_load_lds((gbl_void_t*)src, (lds_void_t*)(tile + ins * 1024),
+                                                 16, 0, 0);
+            }
+        }
+    }
+};
+
 template <int D, int BS>
-__global__ __launch_bounds__(BS * 2) void attn_fwd_kernel(
+__global__ __launch_bounds__(BS * 2, 1) void attn_fwd_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, const int32_t* __restrict__ kv_idx,
     const int32_t* __restrict__ kv_cnt, float scale, uint16_t* __restrict__ o,
     float* __restrict__ lse, int L, int n) {
-    constexpr int NT = BS * 2;       // threads
-    constexpr int KP = D + 8;        // K tile row pitch (elements)
-    constexpr int VP = BS + 8;       // V^T tile row pitch (elements)
-    __shared__ __align__(16) uint16_t Ks[BS * KP];
-    __shared__ __align__(16) uint16_t Vt[D * VP];
+    constexpr int QW = BS / 64;        // q-halves (64 rows each)
+    constexpr int NW = 2 * QW;         // waves
+    constexpr int KVW = BS / 2;        // kv rows per wave per tile
+    constexpr int RT = KVW / 32;       // 32-row kv sub-tiles per wave
+    constexpr int DT = D / 32;         // 32-row d tiles of O^T
+    constexpr int KK = D / 16;         // 16-deep d chunks of S^T
+    constexpr int TILE = BS * D * 2;   // bytes per K or V tile
+    __shared__ __align__(1024) char smem[2 * 2 * TILE];   // [buffer][K, V]
 
     const int item = blockIdx.x;
     const int bh = item / n, i = item % n;
-    const int tid = threadIdx.x, w = tid / 64, lane = tid % 64;
-    const int h = lane / 32, l32 = lane % 32;
+    const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+    const int h = lane >> 5, l32 = lane & 31;
+    const int qw = w % QW, kh = w / QW;
     const size_t base = (size_t)bh * L * D;
-    const int qrow = i * BS + 32 * w + l32;
     const float c2 = scale * kLog2e;
 
-    // Q^T as the B operand: lane holds Q[qrow][16kk + 8h .. +7]
-    bf16x8 qreg[D / 16];
+    // Q^T as the B operand of S^T: lane holds Q[q][16kk + 8h .. +7]
+    bf16x8 qreg[2][KK];
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) {
-        if (qrow < L)
-            qreg[kk] = load_bf16x8(q + base + (size_t)qrow * D + 16 * kk + 8 * h);
-        else
-            qreg[kk] = __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0));
+    for (int qt = 0; qt < 2; ++qt) {
+        const int qrow = i * BS + 64 * qw + 32 * qt + l32;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            uint4 val = make_uint4(0, 0, 0, 0);
+            if (qrow < L)
+                val = *reinterpret_cast<const uint4*>(q + base + (size_t)qrow * D + 16 * kk + 8 * h);
+            qreg[qt][kk] = __builtin_bit_cast(bf16x8, val);
+        }
     }
 
-    f32x16 oacc[D / 32];
+    f32x16 oacc[2][DT];
 #pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt) oacc[dt] = f32x16{};
-    float m = -INFINITY, lsum = 0.0f;
-
-    // Accumulator row rho of a 32-row tile is kv 32*rt + perm(rho): lane
-    // (half h) register ii then holds kv 32*rt + 16*(ii/8) + 8h + (ii%8).
-    const int g4 = l32 / 8, hb = (l32 / 4) % 2, r4 = l32 % 4;
-    const int krow = 16 * (g4 / 2) + 8 * hb + 4 * (g4 % 2) + r4;
+    for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) oacc[qt][dt] = f32x16{};
+    float m[2] = {-INFINITY, -INFINITY};
+    float l[2] = {0.0f, 0.0f};
 
     const int cnt = kv_cnt[item];
     const int32_t* list = kv_idx + (size_t)item * n;
-    for (int t = 0; t < cnt; ++t) {
-        const int j = list[t];
-        const int k0 = j * BS;
-        const int kvalid = min(BS, L - k0);
-        __syncthreads();
-        for (int e = tid; e < BS * (D / 8); e += NT) {
-            const int r = e % BS, c = e / BS;
-            uint4 kv4 = make_uint4(0, 0, 0, 0), vv4 = make_uint4(0, 0, 0, 0);
-            if (r < kvalid) {
-                kv4 = *reinterpret_cast<const uint4*>(k + base + (size_t)(k0 + r) * D + c * 8);
-                vv4 = *reinterpret_cast<const uint4*>(v + base + (size_t)(k0 + r) * D + c * 8);
-            }
-            *reinterpret_cast<uint4*>(Ks + r * KP + c * 8) = kv4;
-            const uint32_t vw[4] = {vv4.x, vv4.y, vv4.z, vv4.w};
-#pragma unroll
-            for (int e2 = 0; e2 < 4; ++e2) {
-                Vt[(c * 8 + 2 * e2) * VP + r] = static_cast<uint16_t>(vw[e2] & 0xFFFFu);
-                Vt[(c * 8 + 2 * e2 + 1) * VP + r] = static_cast<uint16_t>(vw[e2] >> 16);
-            }
-        }
-        __syncthreads();
+    const TileCopy<D, BS, NW> copy(w, lane);
+    if (cnt > 0) {
+        const int j0 = list[0];
+        const int kv0 = min(BS, L - j0 * BS);
+        copy.issue(k + base, j0 * BS, kv0, smem, w, lane);
+        copy.issue(v + base, j0 * BS, kv0, smem + TILE, w, lane);
+    }
 
-        f32x16 sacc[BS / 32];
-#pragma unroll
-        for (int rt = 0; rt < BS / 32; ++rt) {
-            sacc[rt] = f32x16{};
-#pragma unroll
-            for (int kk = 0; kk < D / 16; ++kk) {
-                const bf16x8 a = load_bf16x8(Ks + (32 * rt + krow) * KP + 16 * kk + 8 * h);
-                sacc[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sacc[rt], 0, 0, 0);
-            }
+    // Per-lane LDS byte addresses.  The swizzle of every row a lane reads
+    // depends only on the lane, so an address is a lane constant XOR a
+    // compile-time chunk field, plus a compile-time row offset.
+    constexpr int ROWB = 2 * D;
+    //   K operand (S^T A operand): row kh*KVW + 32 rt + l32, chunk 2 kk + h
+    const int ka = (kh * KVW + l32) * ROWB + ((h ^ swz<D>(l32)) << 4);
+    //   V^T operand (transposing reads): rows kv0 + (lane%16)/4 with
+    //   kv0 = kh*KVW + 16 cc + 4h (+8), d = 32 dt + 16 ((lane/16)&1) + 4 (lane%4)
+    const int s16 = lane & 15, grp = lane >> 4;
+    const int tr_row = 4 * h + (s16 >> 2);
+    const int c0 = 2 * (grp & 1) + ((s16 & 3) >> 1);
+    const int half8 = (s16 & 1) << 3;
+    const int va = (kh * KVW + tr_row) * ROWB + ((c0 ^ swz<D>(tr_row)) << 4) + half8;
+    const int vb = (kh * KVW + tr_row + 8) * ROWB + ((c0 ^ swz<D>(tr_row + 8)) << 4) + half8;
+
+    for (int t = 0; t < cnt; ++t) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        if (t + 1 < cnt) {
+            const int jn = list[t + 1];
+            const int kvn = min(BS, L - jn * BS);
+            char* nb = smem + ((t + 1) & 1) * 2 * TILE;
+            copy.issue(k + base, jn * BS, kvn, nb, w, lane);
+            copy.issue(v + base, jn * BS, kvn, nb + TILE, w, lane);
         }
-        if (kvalid < BS) {
+        const int j = list[t];
+        const int kvalid = min(BS, L - j * BS);
+        const char* Kt = smem + (t & 1) * 2 * TILE;
+        const char* Vt = Kt + TILE;
+
+        // This wave's kv half in 32-row sub-tiles; each sub-tile is one
+        // online-softmax step: S^T = K Q^T, softmax, O^T += V^T P^T.
 #pragma unroll
-            for (int rt = 0; rt < BS / 32; ++rt)
+        for (int rt = 0; rt < RT; ++rt) {
+            f32x16 s[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                const bf16x8 a = __builtin_bit_cast(
+                    bf16x8, *reinterpret_cast<const uint4*>(Kt + ((ka ^ (32 * kk)) + 32 * rt * ROWB)));
+                s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[0][kk], s[0], 0, 0, 0);
+                s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[1][kk], s[1], 0, 0, 0);
+            }
+            if (kvalid < BS) {
 #pragma unroll
                 for (int ii = 0; ii < 16; ++ii) {
-                    const int kv = 32 * rt + 16 * (ii / 8) + 8 * h + (ii % 8);
-                    if (kv >= kvalid) sacc[rt][ii] = -INFINITY;
+                    const int kv = kh * KVW + 32 * rt + 8 * (ii >> 2) + 4 * h + (ii & 3);
+                    if (kv >= kvalid) {
+                        s[0][ii] = -INFINITY;
+                        s[1][ii] = -INFINITY;
+                    }
                 }
-        }
-        float mx = -INFINITY;
-#pragma unroll
-        for (int rt = 0; rt < BS / 32; ++rt)
-#pragma unroll
-            for (int ii = 0; ii < 16; ++ii) mx = fmaxf(mx, sacc[rt][ii]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m, mx);
-        const float alpha = exp2f((m - m_new) * c2);
-        const float mb = m_new * c2;
-        float psum = 0.0f;
-#pragma unroll
-        for (int rt = 0; rt < BS / 32; ++rt)
-#pragma unroll
-            for (int ii = 0; ii < 16; ++ii) {
-                const float p = exp2f(sacc[rt][ii] * c2 - mb);
-                sacc[rt][ii] = p;
-                psum += p;
             }
-        lsum = lsum * alpha + psum;
-        m = m_new;
 #pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
-
+            for (int qt = 0; qt < 2; ++qt) {
+                float mx = -INFINITY;
 #pragma unroll
-        for (int cc = 0; cc < BS / 16; ++cc) {
-            bf16x8 b;
+                for (int ii = 0; ii < 16; ++ii) mx = fmaxf(mx, s[qt][ii]);
+                mx = fmaxf(mx, __shfl_xor(mx, 32));
+                const bool need = (mx - m[qt]) * c2 > kRescaleLog2;
+                const float m_new = need ? mx : m[qt];
+                const float alpha = need ? __builtin_amdgcn_exp2f((m[qt] - mx) * c2) : 1.0f;
+                const float mb = m_new == -INFINITY ? 0.0f : m_new * c2;
+                float ps = 0.0f;
 #pragma unroll
-            for (int e2 = 0; e2 < 8; ++e2) b[e2] = static_cast<__bf16>(sacc[cc / 2][8 * (cc % 2) + e2]);
+                for (int ii = 0; ii < 16; ++ii) {
+                    const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[qt][ii], c2, -mb));
+                    s[qt][ii] = p;
+                    ps += p;
+                }
+                l[qt] = l[qt] * alpha + ps;
+                m[qt] = m_new;
+                if (__any(need)) {
 #pragma unroll
-            for (int dt = 0; dt < D / 32; ++dt) {
-                const bf16x8 a = load_bf16x8(Vt + (32 * dt + l32) * VP + 16 * cc + 8 * h);
-                oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, oacc[dt], 0, 0, 0);
+                    for (int dt = 0; dt < DT; ++dt) oacc[qt][dt] *= alpha;
+                }
+            }
+#pragma unroll
+            for (int c1 = 0; c1 < 2; ++c1) {
+                const int cc = 2 * rt + c1;
+                bf16x8 b[2];
+#pragma unroll
+                for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) b[qt][e] = static_cast<__bf16>(s[qt][8 * c1 + e]);
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+                    const s16x4 ta = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                        (lds_s16x4_t*)(Vt + ((va ^ (64 * dt)) + 16 * cc * ROWB)));
+                    const s16x4 tb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                        (lds_s16x4_t*)(Vt + ((vb ^ (64 * dt)) + 16 * cc * ROWB)));
+                    const s16x8 v8 = {ta[0], ta[1], ta[2], ta[3], tb[0], tb[1], tb[2], tb[3]};
+                    const bf16x8 a = __builtin_bit_cast(bf16x8, v8);
+                    oacc[0][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[0], oacc[0][dt], 0, 0, 0);
+                    oacc[1][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[1], oacc[1][dt], 0, 0, 0);
+                }
             }
         }
     }
 
-    const float ltot = lsum + __shfl_xor(lsum, 32);
-    if (qrow < L) {
-        const float inv = ltot > 0.0f ? 1.0f / ltot : 0.0f;
-        uint16_t* orow = o + base + (size_t)qrow * D;
+    // merge the two kv halves of every q-half through LDS
 #pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt)
+    for (int qt = 0; qt < 2; ++qt) l[qt] += __shfl_xor(l[qt], 32);
+    __syncthreads();
+    float* mo = reinterpret_cast<float*>(smem) + qw * (2 * DT * 16 * 64 + 4 * 64);
+    if (kh == 1) {
 #pragma unroll
-            for (int gq = 0; gq < 4; ++gq) {
-                const int d0 = 32 * dt + 8 * gq + 4 * h;
-                uint16_t vals[4];
+        for (int qt = 0; qt < 2; ++qt) {
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    vals[r] = __builtin_bit_cast(uint16_t,
-                                                 static_cast<__bf16>(oacc[dt][4 * gq + r] * inv));
-                uint2 pk;
-                pk.x = (uint32_t)vals[0] | ((uint32_t)vals[1] << 16);
-                pk.y = (uint32_t)vals[2] | ((uint32_t)vals[3] << 16);
-                *reinterpret_cast<uint2*>(orow + d0) = pk;
-            }
-        if (lse != nullptr && h == 0)
-            lse[(size_t)bh * L + qrow] = cnt > 0 ? m * scale + logf(ltot) : -INFINITY;
+            for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                for (int ii = 0; ii < 16; ++ii) mo[((qt * DT + dt) * 16 + ii) * 64 + lane] = oacc[qt][dt][ii];
+            mo[2 * DT * 16 * 64 + qt * 64 + lane] = m[qt];
+            mo[2 * DT * 16 * 64 + (2 + qt) * 64 + lane] = l[qt];
+        }
     }
+    __syncthreads();
+    if (kh == 0) {
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+            const int qrow = i * BS + 64 * qw + 32 * qt + l32;
+            const float mb = mo[2 * DT * 16 * 64 + qt * 64 + lane];
+            const float lb = mo[2 * DT * 16 * 64 + (2 + qt) * 64 + lane];
+            const float mm = fmaxf(m[qt], mb);
+            const float fa = m[qt] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((m[qt] - mm) * c2);
+            const float fb = mb == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((mb - mm) * c2);
+            const float ltot = l[qt] * fa + lb * fb;
+            const float inv = ltot > 0.0f ? 1.0f / ltot : 0.0f;
+            if (qrow < L) {
+                uint16_t* orow = o + base + (size_t)qrow * D;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                    for (int gq = 0; gq < 4; ++gq) {
+                        uint16_t vals[4];
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int ii = 4 * gq + r;
+                            const float ob = mo[((qt * DT + dt) * 16 + ii) * 64 + lane];
+                            const float val = (oacc[qt][dt][ii] * fa + ob * fb) * inv;
+                            vals[r] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(val));
+                        }
+                        uint2 pk;
+                        pk.x = (uint32_t)vals[0] | ((uint32_t)vals[1] << 16);
+                        pk.y = (uint32_t)vals[2] | ((uint32_t)vals[3] << 16);
+                        *reinterpret_cast<uint2*>(orow + 32 * dt + 8 * gq + 4 * h) = pk;
+                    }
+                if (lse != nullptr && h == 0)
+                    lse[(size_t)bh * L + qrow] = ltot > 0.0f ? mm * scale + logf(ltot) : -INFINITY;
+            }
+        }
+    }
+}
+
+template <int D, int BS>
+hipError_t launch(const uint16_t* q, const uint16_t* k, const uint16_t* v, const int32_t* kv_idx,
+                  const int32_t* kv_cnt, float scale, uint16_t* o, float* lse, int BH, int L, int n,
+                  hipStream_t s) {
+    hipLaunchKernelGGL((attn_fwd_kernel<D, BS>), dim3((unsigned)BH * n), dim3(BS * 2), 0, s, q, k, v,
+                       kv_idx, kv_cnt, scale, o, lse, L, n);
+    return hipGetLastError();
 }
 
 }  // namespace
@@ -178,20 +321,10 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
                            const int32_t* kv_idx, const int32_t* kv_cnt, float scale,
                            uint16_t* o, float* lse, int BH, int L, int d, int bs, int n,
                            hipStream_t s) {
-    const dim3 grid((unsigned)BH * n);
-    if (d == 128 && bs == 128)
-        hipLaunchKernelGGL((attn_fwd_kernel<128, 128>), grid, dim3(256), 0, s, q, k, v, kv_idx,
-                           kv_cnt, scale, o, lse, L, n);
-    else if (d == 128 && bs == 64)
-        hipLaunchKernelGGL((attn_fwd_kernel<128, 64>), grid, dim3(128), 0, s, q, k, v, kv_idx,
-                           kv_cnt, scale, o, lse, L, n);
-    else if (d == 64 && bs == 128)
-        hipLaunchKernelGGL((attn_fwd_kernel<64, 128>), grid, dim3(256), 0, s, q, k, v, kv_idx,
-                           kv_cnt, scale, o, lse, L, n);
-    else
-        hipLaunchKernelGGL((attn_fwd_kernel<64, 64>), grid, dim3(128), 0, s, q, k, v, kv_idx,
-                           kv_cnt, scale, o, lse, L, n);
-    return hipGetLastError();
+    if (d == 128 && bs == 128) return launch<128, 128>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, s);
+    if (d == 128 && bs == 64) return launch<128, 64>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, s);
+    if (d == 64 && bs == 128) return launch<64, 128>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, s);
+    return launch<64, 64>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, s);
 }
 
 }  // namespace moddit
