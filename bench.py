@@ -52,7 +52,22 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=48,
                     help="query blocks of head 0 in the CPU-baseline attention sample")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run one plain device copy of 1 GiB (reference for the HBM "
+                         "byte counters) and exit")
     return ap.parse_args()
+
+
+def calibrate_copy():
+    """One device-to-device copy of exactly 1 GiB through torch's copy kernel;
+    its FETCH_SIZE / WRITE_SIZE readings scale the counters of other kernels."""
+    import torch
+    src = torch.ones(1 << 30, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": 1 << 30}), flush=True)
 
 
 def kept_flops(kv_idx, kv_cnt, L, bs, d):
@@ -122,6 +137,10 @@ def main():
               "the hot path is measured at one GPU's share, see DESIGN.md for sharding.",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
 
     import numpy as np
     import torch

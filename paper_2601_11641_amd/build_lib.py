@@ -20,9 +20,12 @@ ARCH = "gfx950"
 SOURCES = ["predictor.hip", "attn_fwd.hip", "capi.cpp"]
 
 # Packed fp32 VALU forms are kept out of the generated code on purpose.
+# MFMA results are kept in architectural VGPRs (VGPR form) so that the
+# softmax and the accumulator rescale never shuttle them through AGPRs.
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17", "-Wall",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
 ]
 
 

@@ -1,11 +1,12 @@
 // Block-sparse attention forward for gfx950 (Eq. 1 with a block mask).
 //
-// One workgroup per (head, query block i of BS rows).  The workgroup has
-// 2 * BS/64 waves: wave w owns 64 query rows (q-half w % (BS/64)) and one
-// half of every key/value tile (kv-half w / (BS/64)).  Each wave runs its own
-// online softmax over its kv halves; the two partial results of a q-half are
-// merged through LDS at the end.  Splitting the tile this way halves the LDS
-// bytes read per MFMA flop compared with 32-row waves over whole tiles.
+// One workgroup per (head, query block i of BS rows) with 2 * BS/32 waves:
+// wave w owns 32 query rows (slice w % (BS/32)) and one half of every
+// key/value tile (kv half w / (BS/32)).  Each wave runs its own online
+// softmax over its kv halves; the two partial results of a slice are merged
+// through LDS at the end.  With 32-row waves everything a wave needs fits in
+// 256 registers, so two waves share each SIMD and the hardware interleaves
+// one wave's softmax with the other's matrix products.
 //
 // Per kept key block j of the row's list:
 //   * the K and V tiles (BS x D bf16, row-major, 16-byte chunks XOR-swizzled
@@ -62,25 +63,26 @@ struct TileCopy {
     static constexpr int RPI = 64 / LPR;          // rows per 1-KB copy
     static constexpr int IPW = BS * ROWB / 1024 / NW;
     static constexpr int NV = D == 128 ? 4 : 1;
-    int voff[NV];                                  // element offsets, lane part
+    uint32_t voff[NV];                             // byte offsets, lane part
 
-    __device__ __forceinline__ TileCopy(int w, int lane) {
+    __device__ __forceinline__ explicit TileCopy(int lane) {
 #pragma unroll
         for (int a = 0; a < NV; ++a) {
             const int row = a * RPI + lane / LPR;  // row mod 16 (D=128) / mod 8 (D=64)
-            voff[a] = (lane / LPR) * D + (((lane % LPR) ^ swz<D>(row)) << 3);
+            voff[a] = (uint32_t)((lane / LPR) * ROWB + (((lane % LPR) ^ swz<D>(row)) << 4));
         }
-        (void)w;
     }
 
+    // g: first element of the head; k0: first row of the tile; w: wave index
+    // (wave-uniform); tile: LDS destination (wave-uniform).
     __device__ __forceinline__ void issue(const uint16_t* __restrict__ g, int k0, int kvalid,
                                           char* tile, int w, int lane) const {
         if (kvalid == BS) {
-            const uint16_t* gt = g + (size_t)k0 * D;
+            const char* gt = reinterpret_cast<const char*>(g + (size_t)k0 * D);
 #pragma unroll
             for (int ii = 0; ii < IPW; ++ii) {
                 const int ins = w * IPW + ii;
-                const uint16_t* src = gt + ins * RPI * D + voff[ii % NV];
+                const char* src = gt + (size_t)ins * 1024 + voff[ii % NV];
                 __builtin_amdgcn_global_load_lds((gbl_void_t*)src, (lds_void_t*)(tile + ins * 1024),
                                                  16, 0, 0);
             }
@@ -99,53 +101,49 @@ struct TileCopy {
 };
 
 template <int D, int BS>
-__global__ __launch_bounds__(BS * 2, 1) void attn_fwd_kernel(
+__global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, const int32_t* __restrict__ kv_idx,
     const int32_t* __restrict__ kv_cnt, float scale, uint16_t* __restrict__ o,
     float* __restrict__ lse, int L, int n) {
-    constexpr int QW = BS / 64;        // q-halves (64 rows each)
-    constexpr int NW = 2 * QW;         // waves
+    constexpr int QW = BS / 32;        // 32-row query slices
+    constexpr int NW = 2 * QW;         // waves: every slice x two kv halves
     constexpr int KVW = BS / 2;        // kv rows per wave per tile
     constexpr int RT = KVW / 32;       // 32-row kv sub-tiles per wave
     constexpr int DT = D / 32;         // 32-row d tiles of O^T
     constexpr int KK = D / 16;         // 16-deep d chunks of S^T
     constexpr int TILE = BS * D * 2;   // bytes per K or V tile
+    constexpr int ROWB = 2 * D;
     __shared__ __align__(1024) char smem[2 * 2 * TILE];   // [buffer][K, V]
 
     const int item = blockIdx.x;
     const int bh = item / n, i = item % n;
-    const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
     const int h = lane >> 5, l32 = lane & 31;
     const int qw = w % QW, kh = w / QW;
     const size_t base = (size_t)bh * L * D;
     const float c2 = scale * kLog2e;
+    const int qrow = i * BS + 32 * qw + l32;
 
-    // Q^T as the B operand of S^T: lane holds Q[q][16kk + 8h .. +7]
-    bf16x8 qreg[2][KK];
+    // Q^T as the B operand of S^T: lane holds Q[qrow][16kk + 8h .. +7]
+    bf16x8 qreg[KK];
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
-        const int qrow = i * BS + 64 * qw + 32 * qt + l32;
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-            uint4 val = make_uint4(0, 0, 0, 0);
-            if (qrow < L)
-                val = *reinterpret_cast<const uint4*>(q + base + (size_t)qrow * D + 16 * kk + 8 * h);
-            qreg[qt][kk] = __builtin_bit_cast(bf16x8, val);
-        }
+    for (int kk = 0; kk < KK; ++kk) {
+        uint4 val = make_uint4(0, 0, 0, 0);
+        if (qrow < L)
+            val = *reinterpret_cast<const uint4*>(q + base + (size_t)qrow * D + 16 * kk + 8 * h);
+        qreg[kk] = __builtin_bit_cast(bf16x8, val);
     }
 
-    f32x16 oacc[2][DT];
+    f32x16 oacc[DT];
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) oacc[qt][dt] = f32x16{};
-    float m[2] = {-INFINITY, -INFINITY};
-    float l[2] = {0.0f, 0.0f};
+    for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
+    float m = -INFINITY, l = 0.0f;
 
     const int cnt = kv_cnt[item];
     const int32_t* list = kv_idx + (size_t)item * n;
-    const TileCopy<D, BS, NW> copy(w, lane);
+    const TileCopy<D, BS, NW> copy(lane);
     if (cnt > 0) {
         const int j0 = list[0];
         const int kv0 = min(BS, L - j0 * BS);
@@ -156,7 +154,6 @@ __global__ __launch_bounds__(BS * 2, 1) void attn_fwd_kernel(
     // Per-lane LDS byte addresses.  The swizzle of every row a lane reads
     // depends only on the lane, so an address is a lane constant XOR a
     // compile-time chunk field, plus a compile-time row offset.
-    constexpr int ROWB = 2 * D;
     //   K operand (S^T A operand): row kh*KVW + 32 rt + l32, chunk 2 kk + h
     const int ka = (kh * KVW + l32) * ROWB + ((h ^ swz<D>(l32)) << 4);
     //   V^T operand (transposing reads): rows kv0 + (lane%16)/4 with
@@ -167,6 +164,69 @@ __global__ __launch_bounds__(BS * 2, 1) void attn_fwd_kernel(
     const int half8 = (s16 & 1) << 3;
     const int va = (kh * KVW + tr_row) * ROWB + ((c0 ^ swz<D>(tr_row)) << 4) + half8;
     const int vb = (kh * KVW + tr_row + 8) * ROWB + ((c0 ^ swz<D>(tr_row + 8)) << 4) + half8;
+
+    // One kv tile: for each 32-row sub-tile of this wave's half, one online
+    // softmax step.  The rarely taken branches (short tail tile, rescale)
+    // hold an empty volatile asm so the compiler keeps them as branches
+    // instead of turning them into unconditional selects and multiplies.
+    auto tile_step = [&](const char* Kt, const char* Vt, int kvalid) {
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            f32x16 s = f32x16{};
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                const bf16x8 a = __builtin_bit_cast(
+                    bf16x8, *reinterpret_cast<const uint4*>(Kt + ((ka ^ (32 * kk)) + 32 * rt * ROWB)));
+                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], s, 0, 0, 0);
+            }
+            if (kvalid < BS) {
+                asm volatile("" ::: "memory");
+                const int lim = kvalid - (kh * KVW + 32 * rt + 4 * h);
+#pragma unroll
+                for (int ii = 0; ii < 16; ++ii)
+                    s[ii] = (8 * (ii >> 2) + (ii & 3) >= lim) ? -INFINITY : s[ii];
+            }
+            float mx = -INFINITY;
+#pragma unroll
+            for (int ii = 0; ii < 16; ++ii) mx = fmaxf(mx, s[ii]);
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const bool need = (mx - m) * c2 > kRescaleLog2;
+            const float m_new = need ? mx : m;
+            const float alpha = need ? __builtin_amdgcn_exp2f((m - mx) * c2) : 1.0f;
+            const float mb = m_new == -INFINITY ? 0.0f : m_new * c2;
+            float ps = 0.0f;
+#pragma unroll
+            for (int ii = 0; ii < 16; ++ii) {
+                const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[ii], c2, -mb));
+                s[ii] = p;
+                ps += p;
+            }
+            l = l * alpha + ps;
+            m = m_new;
+            if (__any(need)) {
+                asm volatile("" ::: "memory");
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
+            }
+#pragma unroll
+            for (int c1 = 0; c1 < 2; ++c1) {
+                const int cc = 2 * rt + c1;
+                bf16x8 b;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) b[e] = static_cast<__bf16>(s[8 * c1 + e]);
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+                    const s16x4 ta = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                        (lds_s16x4_t*)(Vt + ((va ^ (64 * dt)) + 16 * cc * ROWB)));
+                    const s16x4 tb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                        (lds_s16x4_t*)(Vt + ((vb ^ (64 * dt)) + 16 * cc * ROWB)));
+                    const s16x8 v8 = {ta[0], ta[1], ta[2], ta[3], tb[0], tb[1], tb[2], tb[3]};
+                    oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(bf16x8, v8), b, oacc[dt], 0, 0, 0);
+                }
+            }
+        }
+    };
 
     for (int t = 0; t < cnt; ++t) {
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -181,127 +241,51 @@ __global__ __launch_bounds__(BS * 2, 1) void attn_fwd_kernel(
         const int j = list[t];
         const int kvalid = min(BS, L - j * BS);
         const char* Kt = smem + (t & 1) * 2 * TILE;
-        const char* Vt = Kt + TILE;
-
-        // This wave's kv half in 32-row sub-tiles; each sub-tile is one
-        // online-softmax step: S^T = K Q^T, softmax, O^T += V^T P^T.
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt) {
-            f32x16 s[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-            for (int kk = 0; kk < KK; ++kk) {
-                const bf16x8 a = __builtin_bit_cast(
-                    bf16x8, *reinterpret_cast<const uint4*>(Kt + ((ka ^ (32 * kk)) + 32 * rt * ROWB)));
-                s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[0][kk], s[0], 0, 0, 0);
-                s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[1][kk], s[1], 0, 0, 0);
-            }
-            if (kvalid < BS) {
-#pragma unroll
-                for (int ii = 0; ii < 16; ++ii) {
-                    const int kv = kh * KVW + 32 * rt + 8 * (ii >> 2) + 4 * h + (ii & 3);
-                    if (kv >= kvalid) {
-                        s[0][ii] = -INFINITY;
-                        s[1][ii] = -INFINITY;
-                    }
-                }
-            }
-#pragma unroll
-            for (int qt = 0; qt < 2; ++qt) {
-                float mx = -INFINITY;
-#pragma unroll
-                for (int ii = 0; ii < 16; ++ii) mx = fmaxf(mx, s[qt][ii]);
-                mx = fmaxf(mx, __shfl_xor(mx, 32));
-                const bool need = (mx - m[qt]) * c2 > kRescaleLog2;
-                const float m_new = need ? mx : m[qt];
-                const float alpha = need ? __builtin_amdgcn_exp2f((m[qt] - mx) * c2) : 1.0f;
-                const float mb = m_new == -INFINITY ? 0.0f : m_new * c2;
-                float ps = 0.0f;
-#pragma unroll
-                for (int ii = 0; ii < 16; ++ii) {
-                    const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[qt][ii], c2, -mb));
-                    s[qt][ii] = p;
-                    ps += p;
-                }
-                l[qt] = l[qt] * alpha + ps;
-                m[qt] = m_new;
-                if (__any(need)) {
-#pragma unroll
-                    for (int dt = 0; dt < DT; ++dt) oacc[qt][dt] *= alpha;
-                }
-            }
-#pragma unroll
-            for (int c1 = 0; c1 < 2; ++c1) {
-                const int cc = 2 * rt + c1;
-                bf16x8 b[2];
-#pragma unroll
-                for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) b[qt][e] = static_cast<__bf16>(s[qt][8 * c1 + e]);
-#pragma unroll
-                for (int dt = 0; dt < DT; ++dt) {
-                    const s16x4 ta = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                        (lds_s16x4_t*)(Vt + ((va ^ (64 * dt)) + 16 * cc * ROWB)));
-                    const s16x4 tb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                        (lds_s16x4_t*)(Vt + ((vb ^ (64 * dt)) + 16 * cc * ROWB)));
-                    const s16x8 v8 = {ta[0], ta[1], ta[2], ta[3], tb[0], tb[1], tb[2], tb[3]};
-                    const bf16x8 a = __builtin_bit_cast(bf16x8, v8);
-                    oacc[0][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[0], oacc[0][dt], 0, 0, 0);
-                    oacc[1][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[1], oacc[1][dt], 0, 0, 0);
-                }
-            }
-        }
+        tile_step(Kt, Kt + TILE, kvalid);
     }
 
-    // merge the two kv halves of every q-half through LDS
-#pragma unroll
-    for (int qt = 0; qt < 2; ++qt) l[qt] += __shfl_xor(l[qt], 32);
+    // merge the two kv halves of every query slice through LDS
+    l += __shfl_xor(l, 32);
     __syncthreads();
-    float* mo = reinterpret_cast<float*>(smem) + qw * (2 * DT * 16 * 64 + 4 * 64);
+    float* mo = reinterpret_cast<float*>(smem) + qw * (DT * 16 * 64 + 2 * 64);
     if (kh == 1) {
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
+        for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-                for (int ii = 0; ii < 16; ++ii) mo[((qt * DT + dt) * 16 + ii) * 64 + lane] = oacc[qt][dt][ii];
-            mo[2 * DT * 16 * 64 + qt * 64 + lane] = m[qt];
-            mo[2 * DT * 16 * 64 + (2 + qt) * 64 + lane] = l[qt];
-        }
+            for (int ii = 0; ii < 16; ++ii) mo[(dt * 16 + ii) * 64 + lane] = oacc[dt][ii];
+        mo[DT * 16 * 64 + lane] = m;
+        mo[DT * 16 * 64 + 64 + lane] = l;
     }
     __syncthreads();
     if (kh == 0) {
+        const float mb = mo[DT * 16 * 64 + lane];
+        const float lb = mo[DT * 16 * 64 + 64 + lane];
+        const float mm = fmaxf(m, mb);
+        const float fa = m == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((m - mm) * c2);
+        const float fb = mb == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((mb - mm) * c2);
+        const float ltot = l * fa + lb * fb;
+        const float inv = ltot > 0.0f ? 1.0f / ltot : 0.0f;
+        if (qrow < L) {
+            uint16_t* orow = o + base + (size_t)qrow * D;
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
-            const int qrow = i * BS + 64 * qw + 32 * qt + l32;
-            const float mb = mo[2 * DT * 16 * 64 + qt * 64 + lane];
-            const float lb = mo[2 * DT * 16 * 64 + (2 + qt) * 64 + lane];
-            const float mm = fmaxf(m[qt], mb);
-            const float fa = m[qt] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((m[qt] - mm) * c2);
-            const float fb = mb == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((mb - mm) * c2);
-            const float ltot = l[qt] * fa + lb * fb;
-            const float inv = ltot > 0.0f ? 1.0f / ltot : 0.0f;
-            if (qrow < L) {
-                uint16_t* orow = o + base + (size_t)qrow * D;
+            for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-                for (int dt = 0; dt < DT; ++dt)
+                for (int gq = 0; gq < 4; ++gq) {
+                    uint16_t vals[4];
 #pragma unroll
-                    for (int gq = 0; gq < 4; ++gq) {
-                        uint16_t vals[4];
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            const int ii = 4 * gq + r;
-                            const float ob = mo[((qt * DT + dt) * 16 + ii) * 64 + lane];
-                            const float val = (oacc[qt][dt][ii] * fa + ob * fb) * inv;
-                            vals[r] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(val));
-                        }
-                        uint2 pk;
-                        pk.x = (uint32_t)vals[0] | ((uint32_t)vals[1] << 16);
-                        pk.y = (uint32_t)vals[2] | ((uint32_t)vals[3] << 16);
-                        *reinterpret_cast<uint2*>(orow + 32 * dt + 8 * gq + 4 * h) = pk;
+                    for (int r = 0; r < 4; ++r) {
+                        const int ii = 4 * gq + r;
+                        const float ob = mo[(dt * 16 + ii) * 64 + lane];
+                        const float val = (oacc[dt][ii] * fa + ob * fb) * inv;
+                        vals[r] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(val));
                     }
-                if (lse != nullptr && h == 0)
-                    lse[(size_t)bh * L + qrow] = ltot > 0.0f ? mm * scale + logf(ltot) : -INFINITY;
-            }
+                    uint2 pk;
+                    pk.x = (uint32_t)vals[0] | ((uint32_t)vals[1] << 16);
+                    pk.y = (uint32_t)vals[2] | ((uint32_t)vals[3] << 16);
+                    *reinterpret_cast<uint2*>(orow + 32 * dt + 8 * gq + 4 * h) = pk;
+                }
+            if (lse != nullptr && h == 0)
+                lse[(size_t)bh * L + qrow] = ltot > 0.0f ? mm * scale + logf(ltot) : -INFINITY;
         }
     }
 }
@@ -310,7 +294,7 @@ template <int D, int BS>
 hipError_t launch(const uint16_t* q, const uint16_t* k, const uint16_t* v, const int32_t* kv_idx,
                   const int32_t* kv_cnt, float scale, uint16_t* o, float* lse, int BH, int L, int n,
                   hipStream_t s) {
-    hipLaunchKernelGGL((attn_fwd_kernel<D, BS>), dim3((unsigned)BH * n), dim3(BS * 2), 0, s, q, k, v,
+    hipLaunchKernelGGL((attn_fwd_kernel<D, BS>), dim3((unsigned)BH * n), dim3(BS * 4), 0, s, q, k, v,
                        kv_idx, kv_cnt, scale, o, lse, L, n);
     return hipGetLastError();
 }
