@@ -35,17 +35,30 @@ typedef __attribute__((address_space(1))) void gbl_void_t;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRescaleLog2 = 8.0f;   // lazy-rescale threshold (log2 units)
+constexpr int kXcds = 8;               // accelerator complex dies of an MI355X
 
 // XOR pattern applied to the 16-byte chunk index of a tile row.  The MFMA
-// operand loads read one chunk column of 8 consecutive rows per LDS cycle and
-// the transposing loads read two adjacent chunks of 4 consecutive rows; with
-// this pattern both land on distinct banks.
+// operand loads read one chunk column of 8 (or 16) consecutive rows at a
+// time, so the pattern must differ in its low 3 (4) bits over any 8 (16)
+// aligned consecutive rows; the transposing loads read two adjacent chunks
+// (an even/odd pair) of 4 aligned consecutive rows, so bits 1..2 must differ
+// over any 4 such rows.  swz(r) = (r&3)<<1 | (r>>2)&1 | (r&8) meets both.
+// max(x, x of lane l ^ 32): with x in both operands, v_permlane32_swap
+// returns x[l mod 32] and x[l mod 32 + 32] to lane l, i.e. its own value and
+// its partner's.
+__device__ __forceinline__ float max_across_halves(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 template <int D>
 __device__ __forceinline__ int swz(int row) {
+    const int f = ((row & 3) << 1) | ((row >> 2) & 1);
     if constexpr (D == 128)
-        return (2 * row + ((row >> 3) & 1)) & 15;
+        return f | (row & 8);
     else
-        return (2 * row + ((row >> 2) & 1)) & 7;
+        return f;
 }
 
 // Issue this wave's share of the 1-KB direct-to-LDS copies of one BS x D
@@ -114,10 +127,24 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     constexpr int KK = D / 16;         // 16-deep d chunks of S^T
     constexpr int TILE = BS * D * 2;   // bytes per K or V tile
     constexpr int ROWB = 2 * D;
-    __shared__ __align__(1024) char smem[2 * 2 * TILE];   // [buffer][K, V]
+    // Two tile buffers ([K, V] each) as distinct LDS objects: the loop below
+    // is unrolled by two so that every copy and every read names its buffer
+    // at compile time, which lets the compiler see that the copy into one
+    // buffer never aliases the reads of the other (otherwise it waits for the
+    // prefetch before the first read of every tile).
+    __shared__ __align__(1024) char buf0[2 * TILE];
+    __shared__ __align__(1024) char buf1[2 * TILE];
 
-    const int item = blockIdx.x;
-    const int bh = item / n, i = item % n;
+    // Work-group -> (head, query block): dispatch puts work-group b on XCD
+    // b % 8.  All XCDs work on the same head at a time (its K/V stays in the
+    // shared last-level cache) and each XCD takes a contiguous run of query
+    // blocks (neighbouring rows share K/V blocks, so the XCD's L2 serves
+    // them).  Padding slots past the last block exit at once.
+    const int chunk = (n + kXcds - 1) / kXcds;
+    const int xcd = blockIdx.x % kXcds, r = blockIdx.x / kXcds;
+    const int bh = r / chunk, i = xcd * chunk + r % chunk;
+    if (i >= n) return;
+    const int item = bh * n + i;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
     const int h = lane >> 5, l32 = lane & 31;
@@ -147,8 +174,8 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     if (cnt > 0) {
         const int j0 = list[0];
         const int kv0 = min(BS, L - j0 * BS);
-        copy.issue(k + base, j0 * BS, kv0, smem, w, lane);
-        copy.issue(v + base, j0 * BS, kv0, smem + TILE, w, lane);
+        copy.issue(k + base, j0 * BS, kv0, buf0, w, lane);
+        copy.issue(v + base, j0 * BS, kv0, buf0 + TILE, w, lane);
     }
 
     // Per-lane LDS byte addresses.  The swizzle of every row a lane reads
@@ -166,7 +193,9 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     const int vb = (kh * KVW + tr_row + 8) * ROWB + ((c0 ^ swz<D>(tr_row + 8)) << 4) + half8;
 
     // One kv tile: for each 32-row sub-tile of this wave's half, one online
-    // softmax step.  The rarely taken branches (short tail tile, rescale)
+    // softmax step (S^T = K Q^T, softmax, O^T += V^T P^T).  With two waves
+    // per SIMD in flight, the hardware overlaps one wave's softmax with the
+    // other's products.  The rarely taken branches (short tail tile, rescale)
     // hold an empty volatile asm so the compiler keeps them as branches
     // instead of turning them into unconditional selects and multiplies.
     auto tile_step = [&](const char* Kt, const char* Vt, int kvalid) {
@@ -181,6 +210,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
             }
             if (kvalid < BS) {
                 asm volatile("" ::: "memory");
+                // rows at or past the end of the sequence score -inf
                 const int lim = kvalid - (kh * KVW + 32 * rt + 4 * h);
 #pragma unroll
                 for (int ii = 0; ii < 16; ++ii)
@@ -189,7 +219,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
             float mx = -INFINITY;
 #pragma unroll
             for (int ii = 0; ii < 16; ++ii) mx = fmaxf(mx, s[ii]);
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            mx = max_across_halves(mx);
             const bool need = (mx - m) * c2 > kRescaleLog2;
             const float m_new = need ? mx : m;
             const float alpha = need ? __builtin_amdgcn_exp2f((m - mx) * c2) : 1.0f;
@@ -228,26 +258,28 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
         }
     };
 
-    for (int t = 0; t < cnt; ++t) {
+    // tile t lives in `cur`; the copy of tile t+1 goes to `nxt`
+    auto step = [&](int t, const char* cur, char* nxt) {
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
         if (t + 1 < cnt) {
             const int jn = list[t + 1];
             const int kvn = min(BS, L - jn * BS);
-            char* nb = smem + ((t + 1) & 1) * 2 * TILE;
-            copy.issue(k + base, jn * BS, kvn, nb, w, lane);
-            copy.issue(v + base, jn * BS, kvn, nb + TILE, w, lane);
+            copy.issue(k + base, jn * BS, kvn, nxt, w, lane);
+            copy.issue(v + base, jn * BS, kvn, nxt + TILE, w, lane);
         }
         const int j = list[t];
-        const int kvalid = min(BS, L - j * BS);
-        const char* Kt = smem + (t & 1) * 2 * TILE;
-        tile_step(Kt, Kt + TILE, kvalid);
+        tile_step(cur, cur + TILE, min(BS, L - j * BS));
+    };
+    for (int t = 0; t < cnt; t += 2) {
+        step(t, buf0, buf1);
+        if (t + 1 < cnt) step(t + 1, buf1, buf0);
     }
 
     // merge the two kv halves of every query slice through LDS
     l += __shfl_xor(l, 32);
     __syncthreads();
-    float* mo = reinterpret_cast<float*>(smem) + qw * (DT * 16 * 64 + 2 * 64);
+    float* mo = reinterpret_cast<float*>(buf0) + qw * (DT * 16 * 64 + 2 * 64);
     if (kh == 1) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
@@ -294,7 +326,9 @@ template <int D, int BS>
 hipError_t launch(const uint16_t* q, const uint16_t* k, const uint16_t* v, const int32_t* kv_idx,
                   const int32_t* kv_cnt, float scale, uint16_t* o, float* lse, int BH, int L, int n,
                   hipStream_t s) {
-    hipLaunchKernelGGL((attn_fwd_kernel<D, BS>), dim3((unsigned)BH * n), dim3(BS * 4), 0, s, q, k, v,
+    const unsigned chunk = (unsigned)(n + kXcds - 1) / kXcds;
+    hipLaunchKernelGGL((attn_fwd_kernel<D, BS>), dim3((unsigned)BH * chunk * kXcds), dim3(BS * 4), 0, s,
+                       q, k, v,
                        kv_idx, kv_cnt, scale, o, lse, L, n);
     return hipGetLastError();
 }
