@@ -28,6 +28,21 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+ATTN_SOURCE = os.path.join(ROOT, "paper_2601_11641_amd", "csrc", "attn_fwd.hip")
+COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "attn_fwd_hunyuan720p_counters.json")
+
+# rocprofv3 counter passes behind COUNTER_SUMMARY (one run each, see that file)
+COUNTER_PASSES = {
+    "A": "SQ_INSTS_VALU SQ_INSTS_MFMA SQ_INSTS_LDS SQ_INSTS_SALU SQ_INSTS_VALU_TRANS_F32 "
+         "SQ_WAVES SQ_BUSY_CYCLES SQ_WAVE_CYCLES",
+    "B": "SQ_VALU_MFMA_BUSY_CYCLES SQ_VALU_MFMA_COEXEC_CYCLES SQ_ACTIVE_INST_VALU "
+         "SQ_ACTIVE_INST_LDS SQ_WAIT_INST_LDS SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE SQ_WAIT_ANY "
+         "GRBM_GUI_ACTIVE",
+    "C": "FETCH_SIZE",
+    "D": "WRITE_SIZE TCC_HIT_sum TCC_MISS_sum",
+    "E": "FETCH_SIZE",      # with --calibrate-copy
+    "F": "WRITE_SIZE",      # with --calibrate-copy
+}
 METRIC = "ms/layer + kept-block TFLOP/s (% bf16 MFMA peak) at 720p video shapes"
 
 WORKLOADS = {
@@ -55,7 +70,94 @@ def parse():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run one plain device copy of 1 GiB (reference for the HBM "
                          "byte counters) and exit")
+    ap.add_argument("--counter-summary", metavar="PMC_DIR",
+                    help="summarise rocprofv3 counter passes A..F found under PMC_DIR/<pass>/ "
+                         "into profiles/ and exit")
     return ap.parse_args()
+
+
+def source_digest() -> str:
+    import hashlib
+    with open(ATTN_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def summarize_counters(pmc_dir: str):
+    """Attention-kernel counters and HBM bytes from the rocprofv3 passes.
+
+    FETCH_SIZE / WRITE_SIZE (KiB per dispatch) are scaled by what the same
+    counters read for a plain 1 GiB device copy (bytes moved / bytes read by
+    the counter)."""
+    import csv
+    import glob
+
+    def load(name, match):
+        vals = {}
+        for f in glob.glob(os.path.join(pmc_dir, name, "**", "*counter_collection.csv"),
+                           recursive=True):
+            per = {}
+            for r in csv.DictReader(open(f)):
+                if match(r["Kernel_Name"]):
+                    key = int(r["Dispatch_Id"])
+                    per.setdefault(key, {}).setdefault(r["Counter_Name"], 0.0)
+                    per[key][r["Counter_Name"]] += float(r["Counter_Value"])
+                    per[key]["_ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+            if per:
+                vals.update(per[max(per)])   # the last dispatch (a timed step)
+        return vals
+    attn = lambda k: "attn_fwd_kernel" in k   # noqa: E731
+    copy = lambda k: "copy" in k.lower() or "elementwise" in k   # noqa: E731
+    a = {}
+    for p in "ABCD":
+        a.update(load(p, attn))
+    cf, cw = load("E", copy), load("F", copy)
+    gib = float(1 << 30)
+    fetch_scale = gib / (cf["FETCH_SIZE"] * 1024.0)
+    write_scale = gib / (cw["WRITE_SIZE"] * 1024.0)
+    fetch = a["FETCH_SIZE"] * 1024.0 * fetch_scale
+    write = a["WRITE_SIZE"] * 1024.0 * write_scale
+    xcd_cycles = a["GRBM_GUI_ACTIVE"] / 8.0
+    mf = a["SQ_INSTS_MFMA"]
+    out = {
+        "kernel": "attn_fwd_kernel<128, 128>",
+        "workload": "hunyuan-720p layer, mass budget 0.75 (bench.py --steps 1 --warmup 0)",
+        "attn_source_sha256_16": source_digest(),
+        "commands": [f"rocprofv3 --pmc {COUNTER_PASSES[p]} -d gpurun_out/pmc/{p} -o pmc "
+                     f"--output-format csv -- python3 bench.py "
+                     + ("--calibrate-copy" if p in "EF" else
+                        "--steps 1 --warmup 0 --no-cpu-baseline") for p in "ABCDEF"],
+        "copy_calibration": {"fetch_scale": round(fetch_scale, 4),
+                             "write_scale": round(write_scale, 4)},
+        "hbm_fetch_bytes": round(fetch), "hbm_write_bytes": round(write),
+        "traffic_bytes": round(fetch + write),
+        "mfma_busy_frac": round(a["SQ_VALU_MFMA_BUSY_CYCLES"] / (xcd_cycles * 1024), 4),
+        "mfma_valu_coexec_frac": round(a["SQ_VALU_MFMA_COEXEC_CYCLES"]
+                                       / a["SQ_VALU_MFMA_BUSY_CYCLES"], 4),
+        "valu_per_mfma": round((a["SQ_INSTS_VALU"] - mf) / mf, 3),
+        "lds_per_mfma": round(a["SQ_INSTS_LDS"] / mf, 3),
+        "trans_per_mfma": round(a["SQ_INSTS_VALU_TRANS_F32"] / mf, 3),
+        "lds_bank_conflict_frac": round(a["SQ_LDS_BANK_CONFLICT"] / a["SQ_LDS_IDX_ACTIVE"], 4),
+        "l2_hit_rate": round(a["TCC_HIT_sum"] / (a["TCC_HIT_sum"] + a["TCC_MISS_sum"]), 4),
+        "shader_clock_ghz": round(xcd_cycles / (a["_ns"] * 1e-9) / 1e9, 3),
+        "duration_ms_under_profiler": round(a["_ns"] * 1e-6, 3),
+    }
+    with open(COUNTER_SUMMARY, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out, indent=1))
+
+
+def measured_traffic():
+    """HBM bytes per attention launch from the committed counter summary, or
+    None when the kernel source has changed since the counters were taken."""
+    try:
+        with open(COUNTER_SUMMARY) as f:
+            c = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if c.get("attn_source_sha256_16") != source_digest():
+        return None
+    return c.get("traffic_bytes")
 
 
 def calibrate_copy():
@@ -140,6 +242,9 @@ def main():
 
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.counter_summary:
+        summarize_counters(args.counter_summary)
         return
 
     import numpy as np
@@ -242,7 +347,7 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(),
         },
     }
     if not args.no_cpu_baseline:
