@@ -1,26 +1,32 @@
 // Block-sparse attention forward for gfx950 (Eq. 1 with a block mask).
 //
-// One workgroup per (head, query block i of BS rows) with 2 * BS/32 waves:
-// wave w owns 32 query rows (slice w % (BS/32)) and one half of every
-// key/value tile (kv half w / (BS/32)).  Each wave runs its own online
-// softmax over its kv halves; the two partial results of a slice are merged
-// through LDS at the end.  With 32-row waves everything a wave needs fits in
-// 256 registers, so two waves share each SIMD and the hardware interleaves
-// one wave's softmax with the other's matrix products.
+// One work-group per (head, pair of query blocks 2p, 2p+1) with 2 * BS/32
+// waves in two groups: group g owns query block 2p+g, wave qw of a group owns
+// 32 of its query rows.  Both groups walk the union of the two kv lists, so
+// every K/V tile brought into LDS serves both blocks (a tile missing from one
+// block's list costs that group nothing but the wait).  Every wave runs an
+// online softmax over whole tiles, half a tile (a "unit") at a time.
 //
-// Per kept key block j of the row's list:
-//   * the K and V tiles (BS x D bf16, row-major, 16-byte chunks XOR-swizzled
-//     per row) are brought into LDS with global_load_lds_dwordx4 one tile
-//     ahead (double buffer), so the copy of tile t+1 overlaps compute on t;
-//   * S^T (kv x q) = K . Q^T with v_mfma_f32_32x32x16_bf16: a lane owns one
-//     query column, so the row max and the rescale are per-lane scalars;
-//   * P = exp2(S * scale*log2e - m) in fp32, rounded to bf16 as the B operand
-//     of the next product without moving between lanes;
-//   * O^T (d x q) += V^T . P^T, the V^T operand read from the row-major V
-//     tile with ds_read_b64_tr_b16 (transposing LDS reads).
-// The running max is only moved when a tile's max exceeds it by more than
-// 2^8 in probability units, so most tiles skip the accumulator rescale.
+// Per unit a wave has two phases:
+//   M  S^T (kv x q) = K . Q^T with v_mfma_f32_32x32x16_bf16 (a lane owns one
+//      query column, so the row max and the rescale are per-lane scalars),
+//      and the product of the previous unit, O^T (d x q) += V^T . P^T, whose
+//      V^T operand comes from the row-major V tile through
+//      ds_read_b64_tr_b16 (transposing LDS reads);
+//   X  the softmax step: row max, lazy rescale (the running max only moves
+//      when a tile's max exceeds it by more than 2^8 in probability units),
+//      P = exp2(S * scale*log2e - m) in fp32, rounded to bf16 as the B
+//      operand of the next product without moving between lanes.
+// Waves of the two groups share every SIMD, and group 1 runs one phase behind
+// group 0 with a work-group barrier after every phase: on each SIMD one wave's
+// matrix products overlap the other wave's softmax.
+//
+// K and V tiles (BS x D bf16, row-major, 16-byte chunks XOR-swizzled per row)
+// are copied straight into LDS (global_load_lds_dwordx4) during the X phases,
+// two buffers each: group 0 copies K, group 1 copies V, one tile ahead.
 #include "moddit_internal.h"
+
+#include <type_traits>
 
 namespace moddit {
 namespace {
@@ -29,20 +35,12 @@ typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef short s16x4 __attribute__((__vector_size__(4 * sizeof(short))));
 typedef short s16x8 __attribute__((__vector_size__(8 * sizeof(short))));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
-typedef __attribute__((address_space(1))) void gbl_void_t;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRescaleLog2 = 8.0f;   // lazy-rescale threshold (log2 units)
 constexpr int kXcds = 8;               // accelerator complex dies of an MI355X
 
-// XOR pattern applied to the 16-byte chunk index of a tile row.  The MFMA
-// operand loads read one chunk column of 8 (or 16) consecutive rows at a
-// time, so the pattern must differ in its low 3 (4) bits over any 8 (16)
-// aligned consecutive rows; the transposing loads read two adjacent chunks
-// (an even/odd pair) of 4 aligned consecutive rows, so bits 1..2 must differ
-// over any 4 such rows.  swz(r) = (r&3)<<1 | (r>>2)&1 | (r&8) meets both.
 // max(x, x of lane l ^ 32): with x in both operands, v_permlane32_swap
 // returns x[l mod 32] and x[l mod 32 + 32] to lane l, i.e. its own value and
 // its partner's.
@@ -52,6 +50,26 @@ __device__ __forceinline__ float max_across_halves(float x) {
     return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
+// Direct-to-LDS copy of 16 bytes per lane: lane l writes LDS bytes
+// [lds + 16 l, +16) with the 16 bytes at sbase + voff (sbase wave-uniform,
+// voff the lane's byte offset).  Written as inline assembly so that the
+// compiler's wait-count bookkeeping does not treat the copy as a pending LDS
+// access (it would otherwise turn every later partial LDS wait into a full
+// one); its completion is tracked by vmcnt alone and waited for explicitly
+// before the barrier that publishes the tile.  M0 carries the LDS address;
+// nothing else in this kernel uses M0.
+__device__ __forceinline__ void lds_copy16(const void* sbase, uint32_t voff, const char* lds) {
+    const uint32_t m0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)lds;
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :: "v"(voff), "s"(sbase), "s"(m0) : "memory");
+}
+
+// XOR pattern applied to the 16-byte chunk index of a tile row.  The MFMA
+// operand loads read one chunk column of 8 (or 16) consecutive rows at a
+// time, so the pattern must differ in its low 3 (4) bits over any 8 (16)
+// aligned consecutive rows; the transposing loads read two adjacent chunks
+// (an even/odd pair) of 4 aligned consecutive rows, so bits 1..2 must differ
+// over any 4 such rows.  swz(r) = (r&3)<<1 | (r>>2)&1 | (r&8) meets both.
 template <int D>
 __device__ __forceinline__ int swz(int row) {
     const int f = ((row & 3) << 1) | ((row >> 2) & 1);
@@ -61,14 +79,14 @@ __device__ __forceinline__ int swz(int row) {
         return f;
 }
 
-// Issue this wave's share of the 1-KB direct-to-LDS copies of one BS x D
-// tile.  Copy `ins` fills LDS bytes [ins*1024, +1024): lane l writes the
-// 16-byte chunk at ins*1024 + 16*l, i.e. row ins*RPI + l/LPR, physical
+// A group's direct-to-LDS copies of one BS x D tile (NW waves, IPW 1-KB
+// copies each).  Copy `ins` fills LDS bytes [ins*1024, +1024): lane l writes
+// the 16-byte chunk at ins*1024 + 16*l, i.e. row ins*RPI + l/LPR, physical
 // chunk l % LPR, which holds logical chunk (l % LPR) ^ swz(row).  The
-// per-lane part of the source offset only depends on ins mod 4 (D = 128) or
-// not at all (D = 64); it is precomputed in voff.  Rows past the end of the
-// sequence (short tail tile) re-read the last valid row: their scores are
-// masked and their probabilities are zero.
+// per-lane source offset only depends on ins mod 4 (D = 128) or not at all
+// (D = 64); it is precomputed in voff.  Rows past the end of the sequence
+// (short tail tile) re-read the last valid row: their scores are masked and
+// their probabilities are zero.
 template <int D, int BS, int NW>
 struct TileCopy {
     static constexpr int ROWB = 2 * D;            // bytes per row
@@ -86,29 +104,44 @@ struct TileCopy {
         }
     }
 
-    // g: first element of the head; k0: first row of the tile; w: wave index
-    // (wave-uniform); tile: LDS destination (wave-uniform).
-    __device__ __forceinline__ void issue(const uint16_t* __restrict__ g, int k0, int kvalid,
-                                          char* tile, int w, int lane) const {
-        if (kvalid == BS) {
-            const char* gt = reinterpret_cast<const char*>(g + (size_t)k0 * D);
+    // Copy ii of wave w (within the group) of a full tile whose first row
+    // starts at byte address gt.
+    __device__ __forceinline__ void issue_one(const char* gt, int ii, char* tile, int w) const {
+        const int ins = w * IPW + ii;
+        lds_copy16(gt + (size_t)ins * 1024, voff[ii % NV], tile + ins * 1024);
+    }
+
+    // All copies of wave w of a short tile (kvalid < BS valid rows starting
+    // at row k0 of the head whose first element is g).
+    __device__ __forceinline__ void issue_tail(const uint16_t* __restrict__ g, int k0, int kvalid,
+                                               char* tile, int w, int lane) const {
 #pragma unroll
-            for (int ii = 0; ii < IPW; ++ii) {
-                const int ins = w * IPW + ii;
-                const char* src = gt + (size_t)ins * 1024 + voff[ii % NV];
-                __builtin_amdgcn_global_load_lds((gbl_void_t*)src, (lds_void_t*)(tile + ins * 1024),
-                                                 16, 0, 0);
-            }
-        } else {
+        for (int ii = 0; ii < IPW; ++ii) {
+            const int ins = w * IPW + ii;
+            const int row = ins * RPI + lane / LPR;
+            const int chunk = (lane % LPR) ^ swz<D>(row);
+            const uint32_t off = (uint32_t)((k0 + min(row, kvalid - 1)) * ROWB + chunk * 16);
+            lds_copy16(g, off, tile + ins * 1024);
+        }
+    }
+
+    // Start copying tile j (rows j*BS ..) of head g into `tile`: a full tile
+    // is returned as a source address for issue_one, a short one is issued
+    // at once and nullptr is returned.
+    __device__ __forceinline__ const char* start(const uint16_t* __restrict__ g, int j, int L, char* tile,
+                                                 int w, int lane) const {
+        const int kvalid = min(BS, L - j * BS);
+        if (kvalid == BS) return reinterpret_cast<const char*>(g + (size_t)j * BS * D);
+        issue_tail(g, j * BS, kvalid, tile, w, lane);
+        return nullptr;
+    }
+
+    __device__ __forceinline__ void issue_all(const uint16_t* __restrict__ g, int j, int L, char* tile, int w,
+                                              int lane) const {
+        const char* gt = start(g, j, L, tile, w, lane);
+        if (gt != nullptr) {
 #pragma unroll
-            for (int ii = 0; ii < IPW; ++ii) {
-                const int ins = w * IPW + ii;
-                const int row = ins * RPI + lane / LPR;
-                const int chunk = (lane % LPR) ^ swz<D>(row);
-                const uint16_t* src = g + (size_t)(k0 + min(row, kvalid - 1)) * D + chunk * 8;
-                __builtin_amdgcn_global_load_lds((gbl_void_t*)src, (lds_void_t*)(tile + ins * 1024),
-                                                 16, 0, 0);
-            }
+            for (int ii = 0; ii < IPW; ++ii) issue_one(gt, ii, tile, w);
         }
     }
 };
@@ -119,41 +152,97 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     const uint16_t* __restrict__ v, const int32_t* __restrict__ kv_idx,
     const int32_t* __restrict__ kv_cnt, float scale, uint16_t* __restrict__ o,
     float* __restrict__ lse, int L, int n) {
-    constexpr int QW = BS / 32;        // 32-row query slices
-    constexpr int NW = 2 * QW;         // waves: every slice x two kv halves
-    constexpr int KVW = BS / 2;        // kv rows per wave per tile
-    constexpr int RT = KVW / 32;       // 32-row kv sub-tiles per wave
+    constexpr int QW = BS / 32;        // waves per group = 32-row query slices of a block
+    constexpr int NT = BS * 4;         // threads: two groups of QW waves
+    constexpr int KVW = BS / 2;        // kv rows per unit (half a tile)
+    constexpr int RT = KVW / 32;       // 32-row kv sub-tiles per unit
     constexpr int DT = D / 32;         // 32-row d tiles of O^T
     constexpr int KK = D / 16;         // 16-deep d chunks of S^T
     constexpr int TILE = BS * D * 2;   // bytes per K or V tile
     constexpr int ROWB = 2 * D;
-    // Two tile buffers ([K, V] each) as distinct LDS objects: the loop below
-    // is unrolled by two so that every copy and every read names its buffer
-    // at compile time, which lets the compiler see that the copy into one
-    // buffer never aliases the reads of the other (otherwise it waits for the
-    // prefetch before the first read of every tile).
-    __shared__ __align__(1024) char buf0[2 * TILE];
-    __shared__ __align__(1024) char buf1[2 * TILE];
+    constexpr int HALF = KVW * ROWB;   // bytes per half tile
+    constexpr int JPT = kMaxBlocks / NT;
+    using Copy = TileCopy<D, BS, QW>;
+    constexpr int IPW = Copy::IPW;
+    __shared__ __align__(1024) char kb0[TILE];
+    __shared__ __align__(1024) char kb1[TILE];
+    __shared__ __align__(1024) char vb0[TILE];
+    __shared__ __align__(1024) char vb1[TILE];
+    __shared__ uint32_t ulist[kMaxBlocks];     // union of the two lists: j | membership << 16
+    __shared__ uint8_t umask[kMaxBlocks];
+    __shared__ int wsum[NT / 64];
 
-    // Work-group -> (head, query block): dispatch puts work-group b on XCD
-    // b % 8.  All XCDs work on the same head at a time (its K/V stays in the
-    // shared last-level cache) and each XCD takes a contiguous run of query
-    // blocks (neighbouring rows share K/V blocks, so the XCD's L2 serves
-    // them).  Padding slots past the last block exit at once.
-    const int chunk = (n + kXcds - 1) / kXcds;
+    // Work-group -> (head, pair of query blocks 2p, 2p+1): dispatch puts
+    // work-group b on XCD b % 8; all XCDs work on one head at a time (its K/V
+    // stays in the shared last-level cache) and each takes a contiguous run of
+    // pairs (neighbouring rows share K/V blocks, so the XCD's L2 serves them).
+    // Padding slots exit at once.
+    const int npairs = (n + 1) / 2;
+    const int chunk = (npairs + kXcds - 1) / kXcds;
     const int xcd = blockIdx.x % kXcds, r = blockIdx.x / kXcds;
-    const int bh = r / chunk, i = xcd * chunk + r % chunk;
-    if (i >= n) return;
-    const int item = bh * n + i;
+    const int bh = r / chunk, pr = xcd * chunk + r % chunk;
+    if (pr >= npairs) return;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
     const int h = lane >> 5, l32 = lane & 31;
-    const int qw = w % QW, kh = w / QW;
+    const int qw = w % QW, g = w / QW;          // query slice, group
+    const int i = 2 * pr + g;                   // this group's query block (n: none)
     const size_t base = (size_t)bh * L * D;
     const float c2 = scale * kLog2e;
     const int qrow = i * BS + 32 * qw + l32;
 
-    // Q^T as the B operand of S^T: lane holds Q[qrow][16kk + 8h .. +7]
+    // ---- union of the kv lists of blocks 2p and 2p+1, ascending j ----
+    // (entries outside [0, n) are ignored; a repeated entry counts once)
+    const int i0 = 2 * pr, i1 = 2 * pr + 1;
+    const int cnt0 = kv_cnt[bh * n + i0];
+    const int cnt1 = i1 < n ? kv_cnt[bh * n + i1] : 0;
+    const int32_t* list0 = kv_idx + (size_t)(bh * n + i0) * n;
+    const int32_t* list1 = list0 + n;
+    for (int j = tid; j < n; j += NT) umask[j] = 0;
+    __syncthreads();
+    for (int a = tid; a < cnt0; a += NT) {
+        const int j = list0[a];
+        if ((unsigned)j < (unsigned)n) umask[j] = 1;
+    }
+    __syncthreads();
+    for (int a = tid; a < cnt1; a += NT) {
+        const int j = list1[a];
+        if ((unsigned)j < (unsigned)n) umask[j] |= 2;
+    }
+    __syncthreads();
+    // thread tid compacts entries [tid*JPT, +JPT) after a work-group scan
+    int mine = 0;
+#pragma unroll
+    for (int e = 0; e < JPT; ++e) {
+        const int j = tid * JPT + e;
+        mine += (j < n && umask[j] != 0) ? 1 : 0;
+    }
+    int incl = mine;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(incl, off);
+        if (lane >= off) incl += y;
+    }
+    if (lane == 63) wsum[w] = incl;
+    __syncthreads();
+    int pos = incl - mine, ucnt = 0;
+#pragma unroll
+    for (int ww = 0; ww < NT / 64; ++ww) {
+        pos += ww < w ? wsum[ww] : 0;
+        ucnt += wsum[ww];
+    }
+#pragma unroll
+    for (int e = 0; e < JPT; ++e) {
+        const int j = tid * JPT + e;
+        if (j < n && umask[j] != 0) ulist[pos++] = (uint32_t)j | ((uint32_t)umask[j] << 16);
+    }
+    // The first product (before any unit has been computed) multiplies a
+    // zero P with the second half of the "previous" V buffer: that half
+    // holds zeros rather than whatever the LDS held before.
+    for (int e = tid; e < HALF / 16; e += NT) reinterpret_cast<uint4*>(vb1 + HALF)[e] = make_uint4(0, 0, 0, 0);
+    __syncthreads();   // publishes the union list and the zeroed half
+
+    // ---- Q slice (B operand of S^T): lane holds Q[qrow][16kk + 8h .. +7] ----
     bf16x8 qreg[KK];
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
@@ -162,163 +251,264 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
             val = *reinterpret_cast<const uint4*>(q + base + (size_t)qrow * D + 16 * kk + 8 * h);
         qreg[kk] = __builtin_bit_cast(bf16x8, val);
     }
+    // Q is complete before the tile loop: no wait on the memory counter
+    // (which also counts the tile copies) is left for the loop to inherit.
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) asm volatile("" : "+v"(qreg[kk]));
 
     f32x16 oacc[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
+    f32x16 sacc[RT];
+    bf16x8 pb[2 * RT];   // P of the pending product: zero until a unit is computed
+#pragma unroll
+    for (int c = 0; c < 2 * RT; ++c) pb[c] = bf16x8{};
     float m = -INFINITY, l = 0.0f;
 
-    const int cnt = kv_cnt[item];
-    const int32_t* list = kv_idx + (size_t)item * n;
-    const TileCopy<D, BS, NW> copy(lane);
-    if (cnt > 0) {
-        const int j0 = list[0];
-        const int kv0 = min(BS, L - j0 * BS);
-        copy.issue(k + base, j0 * BS, kv0, buf0, w, lane);
-        copy.issue(v + base, j0 * BS, kv0, buf0 + TILE, w, lane);
-    }
+    const Copy copy(lane);
+    const uint16_t* kg = k + base;
+    const uint16_t* vg = v + base;
 
-    // Per-lane LDS byte addresses.  The swizzle of every row a lane reads
-    // depends only on the lane, so an address is a lane constant XOR a
-    // compile-time chunk field, plus a compile-time row offset.
-    //   K operand (S^T A operand): row kh*KVW + 32 rt + l32, chunk 2 kk + h
-    const int ka = (kh * KVW + l32) * ROWB + ((h ^ swz<D>(l32)) << 4);
-    //   V^T operand (transposing reads): rows kv0 + (lane%16)/4 with
-    //   kv0 = kh*KVW + 16 cc + 4h (+8), d = 32 dt + 16 ((lane/16)&1) + 4 (lane%4)
+    // Per-lane LDS byte offsets within a half tile.  The swizzle of a row
+    // only depends on the row mod 16, so the same offsets serve both halves.
+    //   K operand (S^T A operand): row 32 rt + l32, chunk 2 kk + h
+    const int ka = l32 * ROWB + ((h ^ swz<D>(l32)) << 4);
+    //   V^T operand (transposing reads): rows 16 cc + 4h + (lane%16)/4 (+8),
+    //   d = 32 dt + 16 ((lane/16)&1) + 4 (lane%4)
     const int s16 = lane & 15, grp = lane >> 4;
     const int tr_row = 4 * h + (s16 >> 2);
     const int c0 = 2 * (grp & 1) + ((s16 & 3) >> 1);
     const int half8 = (s16 & 1) << 3;
-    const int va = (kh * KVW + tr_row) * ROWB + ((c0 ^ swz<D>(tr_row)) << 4) + half8;
-    const int vb = (kh * KVW + tr_row + 8) * ROWB + ((c0 ^ swz<D>(tr_row + 8)) << 4) + half8;
+    const int va = tr_row * ROWB + ((c0 ^ swz<D>(tr_row)) << 4) + half8;
+    const int vb = (tr_row + 8) * ROWB + ((c0 ^ swz<D>(tr_row + 8)) << 4) + half8;
 
-    // One kv tile: for each 32-row sub-tile of this wave's half, one online
-    // softmax step (S^T = K Q^T, softmax, O^T += V^T P^T).  With two waves
-    // per SIMD in flight, the hardware overlaps one wave's softmax with the
-    // other's products.  The rarely taken branches (short tail tile, rescale)
-    // hold an empty volatile asm so the compiler keeps them as branches
-    // instead of turning them into unconditional selects and multiplies.
-    auto tile_step = [&](const char* Kt, const char* Vt, int kvalid) {
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt) {
-            f32x16 s = f32x16{};
-#pragma unroll
-            for (int kk = 0; kk < KK; ++kk) {
-                const bf16x8 a = __builtin_bit_cast(
+    auto barrier = [&]() __attribute__((always_inline)) {
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    auto wait_copies = [&]() __attribute__((always_inline)) { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
+
+    using yes = std::true_type;
+
+    // M phase of a unit: S^T = K_half Q^T (Kt: the unit's half tile) and the
+    // product of the previous unit, O^T += V^T P^T (Vp: its half tile).  The
+    // two are independent and interleaved; operand loads run PF steps ahead
+    // of their products.
+    auto mphase = [&](const char* Kt, const char* Vp, auto on_tag) __attribute__((always_inline)) {
+        constexpr bool on = decltype(on_tag)::value;
+        if constexpr (on) {
+            constexpr int NS = RT * KK;
+            constexpr int PF = 2;
+            bf16x8 ak[NS], av[NS];
+            auto load = [&](int s) __attribute__((always_inline)) {
+                const int rt = s / KK, kk = s % KK;
+                ak[s] = __builtin_bit_cast(
                     bf16x8, *reinterpret_cast<const uint4*>(Kt + ((ka ^ (32 * kk)) + 32 * rt * ROWB)));
-                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], s, 0, 0, 0);
+                const int cc = s / DT, dt = s % DT;
+                const s16x4 ta = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_s16x4_t*)(Vp + ((va ^ (64 * dt)) + 16 * cc * ROWB)));
+                const s16x4 tb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_s16x4_t*)(Vp + ((vb ^ (64 * dt)) + 16 * cc * ROWB)));
+                const s16x8 v8 = {ta[0], ta[1], ta[2], ta[3], tb[0], tb[1], tb[2], tb[3]};
+                av[s] = __builtin_bit_cast(bf16x8, v8);
+            };
+#pragma unroll
+            for (int s = 0; s < PF; ++s) load(s);
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                if (s + PF < NS) load(s + PF);
+                const int rt = s / KK, kk = s % KK;
+                sacc[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[s], qreg[kk], kk == 0 ? f32x16{} : sacc[rt],
+                                                                   0, 0, 0);
+                const int cc = s / DT, dt = s % DT;
+                oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[s], pb[cc], oacc[dt], 0, 0, 0);
+                // keep the operand loads PF steps ahead of their products
+                __builtin_amdgcn_sched_barrier(0);
             }
-            if (kvalid < BS) {
-                asm volatile("" ::: "memory");
-                // rows at or past the end of the sequence score -inf
-                const int lim = kvalid - (kh * KVW + 32 * rt + 4 * h);
+            // the products are issued before the phase ends
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) asm volatile("" : "+v"(sacc[rt]));
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) asm volatile("" : "+v"(oacc[dt]));
+        }
+    };
+    // The M phase of a unit runs both products unless neither is needed
+    // (its tile and the previous one are missing from this group's list); an
+    // unneeded one multiplies a zero P, or produces scores nobody reads.
+    auto mphase_if = [&](const char* Kt, const char* Vp, bool s_on, bool pv_on) __attribute__((always_inline)) {
+        if (s_on || pv_on) mphase(Kt, Vp, yes{});
+    };
+    auto zero_p = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int c = 0; c < 2 * RT; ++c) pb[c] = bf16x8{};
+    };
+
+    // X phase of a unit (kv rows half*KVW .. of a tile with kvalid valid
+    // rows): one online-softmax step, P rounded to bf16 in pb.  The copies
+    // cg (a full tile's source, or nullptr) into ct are spread over the
+    // exponentials; register fences keep each group of exponentials ahead of
+    // the next copy.
+    auto xphase = [&](int kvalid, auto half_tag, const char* cg, char* ct) __attribute__((always_inline)) {
+        constexpr int half = decltype(half_tag)::value;
+        if (kvalid < BS) {
+            asm volatile("" ::: "memory");
+            // rows at or past the end of the sequence score -inf
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                const int lim = kvalid - (half * KVW + 32 * rt + 4 * h);
 #pragma unroll
                 for (int ii = 0; ii < 16; ++ii)
-                    s[ii] = (8 * (ii >> 2) + (ii & 3) >= lim) ? -INFINITY : s[ii];
-            }
-            float mx = -INFINITY;
-#pragma unroll
-            for (int ii = 0; ii < 16; ++ii) mx = fmaxf(mx, s[ii]);
-            mx = max_across_halves(mx);
-            const bool need = (mx - m) * c2 > kRescaleLog2;
-            const float m_new = need ? mx : m;
-            const float alpha = need ? __builtin_amdgcn_exp2f((m - mx) * c2) : 1.0f;
-            const float mb = m_new == -INFINITY ? 0.0f : m_new * c2;
-            float ps = 0.0f;
-#pragma unroll
-            for (int ii = 0; ii < 16; ++ii) {
-                const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[ii], c2, -mb));
-                s[ii] = p;
-                ps += p;
-            }
-            l = l * alpha + ps;
-            m = m_new;
-            if (__any(need)) {
-                asm volatile("" ::: "memory");
-#pragma unroll
-                for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
-            }
-#pragma unroll
-            for (int c1 = 0; c1 < 2; ++c1) {
-                const int cc = 2 * rt + c1;
-                bf16x8 b;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) b[e] = static_cast<__bf16>(s[8 * c1 + e]);
-#pragma unroll
-                for (int dt = 0; dt < DT; ++dt) {
-                    const s16x4 ta = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                        (lds_s16x4_t*)(Vt + ((va ^ (64 * dt)) + 16 * cc * ROWB)));
-                    const s16x4 tb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                        (lds_s16x4_t*)(Vt + ((vb ^ (64 * dt)) + 16 * cc * ROWB)));
-                    const s16x8 v8 = {ta[0], ta[1], ta[2], ta[3], tb[0], tb[1], tb[2], tb[3]};
-                    oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        __builtin_bit_cast(bf16x8, v8), b, oacc[dt], 0, 0, 0);
-                }
+                    sacc[rt][ii] = (8 * (ii >> 2) + (ii & 3) >= lim) ? -INFINITY : sacc[rt][ii];
             }
         }
+        // tree of 3-input maxima (short dependency chains)
+        float t1[RT * 6];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+            for (int gq = 0; gq < 5; ++gq)
+                t1[6 * rt + gq] = fmaxf(sacc[rt][3 * gq], fmaxf(sacc[rt][3 * gq + 1], sacc[rt][3 * gq + 2]));
+            t1[6 * rt + 5] = sacc[rt][15];
+        }
+        float mx;
+        if constexpr (RT == 2) {
+            const float u0 = fmaxf(t1[0], fmaxf(t1[1], t1[2]));
+            const float u1 = fmaxf(t1[3], fmaxf(t1[4], t1[5]));
+            const float u2 = fmaxf(t1[6], fmaxf(t1[7], t1[8]));
+            const float u3 = fmaxf(t1[9], fmaxf(t1[10], t1[11]));
+            mx = fmaxf(fmaxf(u0, u1), fmaxf(u2, u3));
+        } else {
+            mx = fmaxf(fmaxf(t1[0], fmaxf(t1[1], t1[2])), fmaxf(t1[3], fmaxf(t1[4], t1[5])));
+        }
+        mx = max_across_halves(mx);
+        const bool need = (mx - m) * c2 > kRescaleLog2;
+        const float m_new = need ? mx : m;
+        const float alpha = need ? __builtin_amdgcn_exp2f((m - mx) * c2) : 1.0f;
+        const float mb = m_new == -INFINITY ? 0.0f : m_new * c2;
+        if (__any(need)) {
+            asm volatile("" ::: "memory");
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
+        }
+        constexpr int NE = RT * 16;
+        static_assert(NE % IPW == 0, "copies must spread evenly over the exponentials");
+        float ps0 = 0.0f, ps1 = 0.0f;
+#pragma unroll
+        for (int qq = 0; qq < NE; ++qq) {
+            if (cg != nullptr && qq % (NE / IPW) == 0) copy.issue_one(cg, qq / (NE / IPW), ct, qw);
+            const int rt = qq / 16, c1 = (qq / 8) % 2, e = qq % 8;
+            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[rt][8 * c1 + e], c2, -mb));
+            pb[2 * rt + c1][e] = static_cast<__bf16>(p);
+            if (qq % 2 == 0)
+                ps0 += p;
+            else
+                ps1 += p;
+            if (qq % (NE / IPW) == NE / IPW - 1)
+                asm volatile("" : "+v"(pb[2 * rt + c1]), "+v"(ps0), "+v"(ps1));
+        }
+        l = l * alpha + (ps0 + ps1);
+        m = m_new;
+#pragma unroll
+        for (int c = 0; c < 2 * RT; ++c) asm volatile("" : "+v"(pb[c]));
+        asm volatile("" : "+v"(l), "+v"(m));
     };
 
-    // tile t lives in `cur`; the copy of tile t+1 goes to `nxt`
-    auto step = [&](int t, const char* cur, char* nxt) {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
-        if (t + 1 < cnt) {
-            const int jn = list[t + 1];
-            const int kvn = min(BS, L - jn * BS);
-            copy.issue(k + base, jn * BS, kvn, nxt, w, lane);
-            copy.issue(v + base, jn * BS, kvn, nxt + TILE, w, lane);
+    // ---- schedule ----
+    // Slot s: group 0 runs phase s, group 1 runs phase s-1 (M and X
+    // alternate), then a barrier.  Tile t (K(t) in kc, V(t) in vc) is read
+    // by group 0 in the M phases of slots 4t and 4t+2 (V(t) in 4t+2 and
+    // 4t+4) and by group 1 one slot later.  During X of its first unit of
+    // tile t, group 0 copies K(t+1) into kn (last read in slot 4t-1) and
+    // waits for it at the end of the tile (slot 4t+3); group 1 copies V(t+1)
+    // into vp (last read in slot 4t+1) and waits for it at the end of its
+    // next M phase (slot 4t+5).
+    uint32_t e_cur = ucnt > 0 ? ulist[0] : 0u;
+    uint32_t e_nxt = ucnt > 1 ? ulist[1] : 0u;
+    e_cur = __builtin_amdgcn_readfirstlane(e_cur);
+    e_nxt = __builtin_amdgcn_readfirstlane(e_nxt);
+    if (ucnt > 0) copy.issue_all(g == 0 ? kg : vg, (int)(e_cur & 0xFFFF), L, g == 0 ? kb0 : vb0, qw, lane);
+    wait_copies();
+    barrier();
+    if (g == 1) barrier();   // group 1 starts one phase late
+
+    bool prev_active = false;   // the previous tile is in this group's list
+    auto tile = [&](int t, char* kc, char* kn, char* vc, char* vp) __attribute__((always_inline)) {
+        const bool more = t + 1 < ucnt;
+        const int jc = (int)(e_cur & 0xFFFF), jn = (int)(e_nxt & 0xFFFF);
+        const bool active = ((e_cur >> (16 + g)) & 1u) != 0;
+        const int kvalid = min(BS, L - jc * BS);
+        // first half: S from K(t) rows [0, KVW); product of V(t-1) rows [KVW, BS)
+        mphase_if(kc, vp + HALF, active, prev_active);
+        if (g == 1) wait_copies();
+        barrier();
+        // copy of the next tile (a short one is issued at once by start())
+        char* ct = g == 0 ? kn : vp;
+        const char* cg = more ? copy.start(g == 0 ? kg : vg, jn, L, ct, qw, lane) : nullptr;
+        if (active) {
+            xphase(kvalid, std::integral_constant<int, 0>{}, cg, ct);
+        } else {
+            zero_p();
+            if (cg != nullptr) {
+#pragma unroll
+                for (int ii = 0; ii < IPW; ++ii) copy.issue_one(cg, ii, ct, qw);
+            }
         }
-        const int j = list[t];
-        tile_step(cur, cur + TILE, min(BS, L - j * BS));
+        barrier();
+        // second half: S from K(t) rows [KVW, BS); product of V(t) rows [0, KVW)
+        mphase_if(kc + HALF, vc, active, active);
+        barrier();
+        uint32_t e_after = t + 2 < ucnt ? ulist[t + 2] : 0u;
+        e_after = __builtin_amdgcn_readfirstlane(e_after);
+        if (active)
+            xphase(kvalid, std::integral_constant<int, 1>{}, nullptr, ct);
+        else
+            zero_p();
+        if (g == 0) wait_copies();
+        barrier();
+        prev_active = active;
+        e_cur = e_nxt;
+        e_nxt = e_after;
     };
-    for (int t = 0; t < cnt; t += 2) {
-        step(t, buf0, buf1);
-        if (t + 1 < cnt) step(t + 1, buf1, buf0);
+    // The copies are inline assembly, invisible to the compiler's alias
+    // analysis, so the buffers simply rotate at run time.
+    char* kc = kb0;
+    char* kn = kb1;
+    char* vc = vb0;
+    char* vp = vb1;
+    for (int t = 0; t < ucnt; ++t) {
+        tile(t, kc, kn, vc, vp);
+        char* tmp = kc;
+        kc = kn;
+        kn = tmp;
+        tmp = vc;
+        vc = vp;
+        vp = tmp;
     }
+    // the pending product of the last tile's second half (its V now in vp)
+    if (prev_active) mphase(kc, vp + HALF, yes{});
+    if (g == 0) barrier();   // both groups pass the same number of barriers
 
-    // merge the two kv halves of every query slice through LDS
+    // ---- output: this wave owns 32 complete query rows ----
     l += __shfl_xor(l, 32);
-    __syncthreads();
-    float* mo = reinterpret_cast<float*>(buf0) + qw * (DT * 16 * 64 + 2 * 64);
-    if (kh == 1) {
+    if (i < n && qrow < L) {
+        const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+        uint16_t* orow = o + base + (size_t)qrow * D;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-            for (int ii = 0; ii < 16; ++ii) mo[(dt * 16 + ii) * 64 + lane] = oacc[dt][ii];
-        mo[DT * 16 * 64 + lane] = m;
-        mo[DT * 16 * 64 + 64 + lane] = l;
-    }
-    __syncthreads();
-    if (kh == 0) {
-        const float mb = mo[DT * 16 * 64 + lane];
-        const float lb = mo[DT * 16 * 64 + 64 + lane];
-        const float mm = fmaxf(m, mb);
-        const float fa = m == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((m - mm) * c2);
-        const float fb = mb == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((mb - mm) * c2);
-        const float ltot = l * fa + lb * fb;
-        const float inv = ltot > 0.0f ? 1.0f / ltot : 0.0f;
-        if (qrow < L) {
-            uint16_t* orow = o + base + (size_t)qrow * D;
+            for (int gq = 0; gq < 4; ++gq) {
+                uint16_t vals[4];
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-                for (int gq = 0; gq < 4; ++gq) {
-                    uint16_t vals[4];
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int ii = 4 * gq + r;
-                        const float ob = mo[(dt * 16 + ii) * 64 + lane];
-                        const float val = (oacc[dt][ii] * fa + ob * fb) * inv;
-                        vals[r] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(val));
-                    }
-                    uint2 pk;
-                    pk.x = (uint32_t)vals[0] | ((uint32_t)vals[1] << 16);
-                    pk.y = (uint32_t)vals[2] | ((uint32_t)vals[3] << 16);
-                    *reinterpret_cast<uint2*>(orow + 32 * dt + 8 * gq + 4 * h) = pk;
-                }
-            if (lse != nullptr && h == 0)
-                lse[(size_t)bh * L + qrow] = ltot > 0.0f ? mm * scale + logf(ltot) : -INFINITY;
-        }
+                for (int rr = 0; rr < 4; ++rr)
+                    vals[rr] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(oacc[dt][4 * gq + rr] * inv));
+                uint2 pk;
+                pk.x = (uint32_t)vals[0] | ((uint32_t)vals[1] << 16);
+                pk.y = (uint32_t)vals[2] | ((uint32_t)vals[3] << 16);
+                *reinterpret_cast<uint2*>(orow + 32 * dt + 8 * gq + 4 * h) = pk;
+            }
+        if (lse != nullptr && h == 0)
+            lse[(size_t)bh * L + qrow] = l > 0.0f ? m * scale + logf(l) : -INFINITY;
     }
 }
 
@@ -326,10 +516,10 @@ template <int D, int BS>
 hipError_t launch(const uint16_t* q, const uint16_t* k, const uint16_t* v, const int32_t* kv_idx,
                   const int32_t* kv_cnt, float scale, uint16_t* o, float* lse, int BH, int L, int n,
                   hipStream_t s) {
-    const unsigned chunk = (unsigned)(n + kXcds - 1) / kXcds;
+    const unsigned npairs = (unsigned)(n + 1) / 2;
+    const unsigned chunk = (npairs + kXcds - 1) / kXcds;
     hipLaunchKernelGGL((attn_fwd_kernel<D, BS>), dim3((unsigned)BH * chunk * kXcds), dim3(BS * 4), 0, s,
-                       q, k, v,
-                       kv_idx, kv_cnt, scale, o, lse, L, n);
+                       q, k, v, kv_idx, kv_cnt, scale, o, lse, L, n);
     return hipGetLastError();
 }
 
