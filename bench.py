@@ -70,6 +70,14 @@ def parse():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run one plain device copy of 1 GiB (reference for the HBM "
                          "byte counters) and exit")
+    ap.add_argument("--sweep", action="store_true",
+                    help="Wan 720p layer at TOPK densities 0.5/0.25/0.10/0.05: attention time, "
+                         "kept work, per-head imbalance and a linear time model; one JSON line "
+                         "per density and one for the fit")
+    ap.add_argument("--schedule", action="store_true",
+                    help="50-step denoising schedule on the Hunyuan 720p shape (5 dense warm-up "
+                         "steps, 45 predicted sparse steps) for re-anchor intervals 10 and 1; one "
+                         "JSON line per interval")
     ap.add_argument("--counter-summary", metavar="PMC_DIR",
                     help="summarise rocprofv3 counter passes A..F found under PMC_DIR/<pass>/ "
                          "into profiles/ and exit")
@@ -207,18 +215,29 @@ def cpu_baseline(cfg, host, rows_h0, mode, val, total_flops, sample_rows):
     P.collect(q, k, WARMUP_M)
     budget = O.Budget(mode, density=val if mode == "topk" else 1.0,
                       mass=val if mode == "mass" else 1.0)
-    t0 = time.perf_counter()
-    P.predict(q, k, WARMUP_M + 1, budget)
-    t_pred = time.perf_counter() - t0
     n = P.n
     rows = [int(r) for r in np.linspace(0, n - 1, min(sample_rows, n)).round()]
-    t0 = time.perf_counter()
-    O.attention(q[0, 0], k[0, 0], v, rows_h0, cfg.block, 1.0 / math.sqrt(cfg.d), rows=rows)
-    t_attn = time.perf_counter() - t0
     sizes = O.block_sizes(cfg.L, cfg.block)
     sflops = 4.0 * cfg.d * sum(int(sizes[i]) * int(sizes[np.asarray(rows_h0[i])].sum())
                                for i in rows)
-    t_layer = cfg.B * cfg.H * t_pred + t_attn * total_flops / sflops
+
+    def timed(step):
+        t0 = time.perf_counter()
+        P.predict(q, k, step, budget)
+        t_pred = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        O.attention(q[0, 0], k[0, 0], v, rows_h0, cfg.block, 1.0 / math.sqrt(cfg.d), rows=rows)
+        t_attn = time.perf_counter() - t0
+        return t_pred, t_attn, cfg.B * cfg.H * t_pred + t_attn * total_flops / sflops
+
+    t_pred, t_attn, t_layer = timed(WARMUP_M + 1)
+    one_thread = None
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            one_thread = timed(WARMUP_M + 2)[2]
+    except Exception:
+        pass
     return {
         "value": total_flops / t_layer / 1e12,
         "unit": "TFLOP/s",
@@ -227,8 +246,171 @@ def cpu_baseline(cfg, host, rows_h0, mode, val, total_flops, sample_rows):
         "sample": (f"fp64 numpy oracle on head 0: one re-anchor predict step "
                    f"({t_pred:.2f} s, scaled x{cfg.B * cfg.H} heads) + attention of {len(rows)} "
                    f"of {n} query blocks ({t_attn:.2f} s, scaled by kept flops); "
-                   f"layer estimate {t_layer:.1f} s"),
+                   f"layer estimate {t_layer:.1f} s"
+                   + (f"; with 1 BLAS thread {one_thread:.1f} s ({total_flops / one_thread / 1e12:.4f} "
+                      f"TFLOP/s)" if one_thread else "")),
     }
+
+
+def _median_ms(fn, reps, stream):
+    import numpy as np
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(reps)]
+    for a, b in evs:
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return float(np.median([a.elapsed_time(b) for a, b in evs]))
+
+
+def run_sweep(args):
+    """Wan 720p density sweep (TOPK): attention ms and kept work per density,
+    per-head kept-work imbalance (max / mean over heads), and the least-squares
+    model t_attn = a + b * kept TFLOP across the densities."""
+    import numpy as np
+    import torch
+
+    import paper_2601_11641_amd as M
+    import workloads as W
+
+    cfg = W.CONFIGS["wan"]
+    host = W.generate(cfg)
+    dev = torch.device("cuda:0")
+    qd, kd, vd = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev) for x in host)
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    stream = torch.cuda.current_stream()
+    out = torch.empty_like(qd)
+    rows = []
+    for dens in (0.50, 0.25, 0.10, 0.05):
+        st = M.Stats(shape, M.make_params(warmup_m=WARMUP_M, delta_t=1))
+        n = st.n
+        kv_idx = torch.empty((cfg.B, cfg.H, n, n), dtype=torch.int32, device=dev)
+        kv_cnt = torch.empty((cfg.B, cfg.H, n), dtype=torch.int32, device=dev)
+        M.mod_collect_stats(st.handle, qd, kd, WARMUP_M - 1)
+        M.mod_collect_stats(st.handle, qd, kd, WARMUP_M)
+        budget = M.make_budget("topk", density=dens)
+        step = [WARMUP_M]
+
+        def predict():
+            step[0] += 1               # delta_t = 1: every call re-anchors at a new step
+            M.mod_predict_block_mask(st.handle, qd, kd, step[0], budget, kv_idx, kv_cnt, stream)
+        pred_ms = _median_ms(predict, 5, stream)
+        attn = lambda: M.mod_block_sparse_attn_fwd(shape, qd, kd, vd, kv_idx, kv_cnt, 0.0, out,  # noqa: E731
+                                                   None, None, 0, stream)
+        for _ in range(args.warmup):
+            attn()
+        attn_ms = _median_ms(attn, max(args.steps, 5), stream)
+        per_head = np.array([kept_flops(kv_idx[:, h:h + 1], kv_cnt[:, h:h + 1], cfg.L, cfg.block, cfg.d)
+                             for h in range(cfg.H)])
+        flops = float(per_head.sum())
+        rows.append((flops / 1e12, attn_ms))
+        line = {"workload": "wan-720p layer: B=1 H=40 L=75600 d=128 block=128", "budget": f"topk {dens}",
+                "k_blocks": int(kv_cnt[0, 0, 0].item()), "kept_tflop": round(flops / 1e12, 3),
+                "predict_ms": round(pred_ms, 3), "attn_ms": round(attn_ms, 3),
+                "attn_tflops": round(flops / (attn_ms * 1e-3) / 1e12, 1),
+                "head_imbalance": round(float(per_head.max() / per_head.mean()), 3)}
+        print(json.dumps(line), flush=True)
+        st.close()
+    x = np.array([r[0] for r in rows])
+    y = np.array([r[1] for r in rows])
+    A = np.stack([np.ones_like(x), x], 1)
+    (a, b), *_ = np.linalg.lstsq(A, y, rcond=None)
+    pred = a + b * x
+    r2 = 1.0 - float(((y - pred) ** 2).sum() / ((y - y.mean()) ** 2).sum())
+    print(json.dumps({"fit": "attn_ms = a + b * kept_tflop", "a_ms": round(float(a), 3),
+                      "b_ms_per_tflop": round(float(b), 4), "r2": round(r2, 5),
+                      "marginal_tflops": round(1e3 / float(b), 1)}), flush=True)
+
+
+def run_schedule(args):
+    """50 denoising steps on the Hunyuan 720p shape: steps 1-5 dense (full
+    lists) with statistics collected at steps 4 and 5, steps 6-50 predicted
+    masks (mass 0.75) + block-sparse attention; inputs drift between two draws
+    (seeds 1005, 1006) as Q_t = cos(theta_t) Q0 + sin(theta_t) Q1 (same for K).
+    Run for re-anchor intervals 10 and 1."""
+    import numpy as np
+    import torch
+
+    import paper_2601_11641_amd as M
+    import workloads as W
+
+    T = 50
+    cfg = W.CONFIGS["hunyuan"]
+    dev = torch.device("cuda:0")
+    to_dev = lambda x: torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev)  # noqa: E731
+    d0 = W.generate_heads(cfg, seed=1005)
+    d1 = W.generate_heads(cfg, seed=1006)
+    q0, k0, v0 = (to_dev(x) for x in d0)
+    q1, k1 = to_dev(d1[0]), to_dev(d1[1])
+    del d0, d1
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    stream = torch.cuda.current_stream()
+    out = torch.empty_like(q0)
+    n = cfg.n
+    full_idx = torch.arange(n, dtype=torch.int32, device=dev).repeat(cfg.B * cfg.H * n).reshape(
+        cfg.B, cfg.H, n, n)
+    full_cnt = torch.full((cfg.B, cfg.H, n), n, dtype=torch.int32, device=dev)
+    budget = M.make_budget("mass", mass=0.75)
+
+    def inputs(t):
+        th = 0.5 * math.pi * (t - 1) / (T - 1)
+        c, s_ = math.cos(th), math.sin(th)
+        return ((c * q0.float() + s_ * q1.float()).to(torch.bfloat16),
+                (c * k0.float() + s_ * k1.float()).to(torch.bfloat16))
+
+    for dt in (10, 1):
+        st = M.Stats(shape, M.make_params(warmup_m=WARMUP_M, delta_t=dt))
+        kv_idx = torch.empty((cfg.B, cfg.H, n, n), dtype=torch.int32, device=dev)
+        kv_cnt = torch.empty((cfg.B, cfg.H, n), dtype=torch.int32, device=dev)
+        dense_ms, sparse_ms, pred_anchor, pred_other, collect_ms, dens = [], [], [], [], [], []
+        for t in range(1, T + 1):
+            qt, kt = inputs(t)
+            torch.cuda.synchronize()
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            if t <= WARMUP_M:
+                e[0].record(stream)
+                M.mod_block_sparse_attn_fwd(shape, qt, kt, v0, full_idx, full_cnt, 0.0, out, None, None, 0,
+                                            stream)
+                e[1].record(stream)
+                if t >= WARMUP_M - 1:
+                    M.mod_collect_stats(st.handle, qt, kt, t, stream)
+                e[2].record(stream)
+                torch.cuda.synchronize()
+                dense_ms.append(e[0].elapsed_time(e[1]))
+                if t >= WARMUP_M - 1:
+                    collect_ms.append(e[1].elapsed_time(e[2]))
+            else:
+                anchor = (t - WARMUP_M) % dt == 0
+                e[0].record(stream)
+                M.mod_predict_block_mask(st.handle, qt, kt, t, budget, kv_idx, kv_cnt, stream)
+                e[1].record(stream)
+                M.mod_block_sparse_attn_fwd(shape, qt, kt, v0, kv_idx, kv_cnt, 0.0, out, None, None, 0, stream)
+                e[2].record(stream)
+                torch.cuda.synchronize()
+                (pred_anchor if anchor else pred_other).append(e[0].elapsed_time(e[1]))
+                sparse_ms.append(e[1].elapsed_time(e[2]))
+                dens.append(kept_flops(kv_idx, kv_cnt, cfg.L, cfg.block, cfg.d)
+                            / (4.0 * cfg.d * cfg.L * cfg.L * cfg.B * cfg.H))
+        st.close()
+        total_attn = sum(dense_ms) + sum(sparse_ms)
+        total_pred = sum(pred_anchor) + sum(pred_other) + sum(collect_ms)
+        print(json.dumps({
+            "workload": "hunyuan-720p 50-step schedule (B=1 H=24 L=118800 d=128 block=128), mass 0.75",
+            "delta_t": dt, "steps": T, "dense_steps": WARMUP_M,
+            "dense_attn_ms_avg": round(float(np.mean(dense_ms)), 3),
+            "sparse_attn_ms_avg": round(float(np.mean(sparse_ms)), 3),
+            "kept_density_avg": round(float(np.mean(dens)), 4),
+            "kept_density_range": [round(float(min(dens)), 4), round(float(max(dens)), 4)],
+            "collect_ms_avg": round(float(np.mean(collect_ms)), 3),
+            "predict_anchor_ms_avg": round(float(np.mean(pred_anchor)), 3) if pred_anchor else None,
+            "predict_other_ms_avg": round(float(np.mean(pred_other)), 3) if pred_other else None,
+            "anchor_steps": len(pred_anchor),
+            "total_attn_ms": round(total_attn, 1), "total_predictor_ms": round(total_pred, 1),
+            "predictor_share": round(total_pred / (total_attn + total_pred), 4),
+            "all_dense_attn_ms": round(float(np.mean(dense_ms)) * T, 1),
+        }), flush=True)
 
 
 def main():
@@ -245,6 +427,12 @@ def main():
         return
     if args.counter_summary:
         summarize_counters(args.counter_summary)
+        return
+    if args.sweep:
+        run_sweep(args)
+        return
+    if args.schedule:
+        run_schedule(args)
         return
 
     import numpy as np
@@ -347,7 +535,7 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
-            "traffic": measured_traffic(),
+            "traffic": measured_traffic() if args.workload == "hunyuan-720p" else None,
         },
     }
     if not args.no_cpu_baseline:
