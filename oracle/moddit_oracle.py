@@ -382,6 +382,36 @@ def select_row_mass(sig_row: np.ndarray, forced_row: np.ndarray, tau: float) -> 
     return RowSelection(kept, gap, margin)
 
 
+def pattern_values(ctil: np.ndarray, dtil: np.ndarray) -> np.ndarray:
+    """The 3n - 1 predicted pattern intensities in pattern order: diagonals
+    delta = -(n-1) .. n-1 (index delta + n - 1), then columns j (index
+    2n - 1 + j)."""
+    return np.concatenate([np.asarray(ctil, dtype=np.float64), np.asarray(dtil, dtype=np.float64)])
+
+
+def select_patterns(ctil: np.ndarray, dtil: np.ndarray, n: int, K: int, forced: np.ndarray):
+    """Section 5.3, pattern form of the mask: rank the predicted intensities
+    of the parallel-diagonal and vertical patterns together, keep the K
+    largest, and keep block (i, j) iff its diagonal j - i or its column j is
+    among them, or it lies in the forced block-diagonal support K_E.  Keys
+    are taken at float32 precision, ties by pattern index (reading).  The
+    ranking depends on the gauge of (c, d); the minimum-norm solution is
+    used.  Rows that no kept pattern reaches keep nothing.  Returns one
+    RowSelection per query block; key_gap is the head's boundary gap (the
+    K-th minus the (K+1)-th key, inf when K covers every pattern)."""
+    vals = pattern_values(ctil, dtil).astype(np.float32).astype(np.float64)
+    P = vals.size
+    K = int(min(P, max(1, K)))
+    order = np.lexsort((np.arange(P), -vals))
+    chosen = np.zeros(P, dtype=bool)
+    chosen[order[:K]] = True
+    gap = math.inf if K == P else float(vals[order[K - 1]] - vals[order[K]])
+    diag, col = chosen[:2 * n - 1], chosen[2 * n - 1:]
+    i, j = np.indices((n, n))
+    keep = diag[j - i + n - 1] | col[j] | forced
+    return [RowSelection(np.flatnonzero(keep[r]), gap, math.inf) for r in range(n)]
+
+
 def select(sig: np.ndarray, forced: np.ndarray, mode: str, density: float = 1.0,
            mass: float = 1.0):
     """Per-row selection over an n x n score map.  Returns a list of
@@ -439,9 +469,10 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, kept_lists, bs: int,
 
 @dataclass
 class Budget:
-    mode: str = "topk"        # "topk" | "mass"
+    mode: str = "topk"        # "topk" | "mass" | "pattern"
     density: float = 1.0      # TOPK: rho
     mass: float = 1.0         # MASS: tau
+    patterns: int = 1         # PATTERN: K patterns per head
 
 
 class Predictor:
@@ -532,8 +563,11 @@ class Predictor:
             row = []
             for h in range(self.H):
                 ct, dt_ = pred[b][h]
-                sig = scores(ct, dt_, self.n)
                 forced = forced_mask(self.n, self.regions, bool(self.gates[b, h]))
+                if budget.mode == "pattern":
+                    row.append(select_patterns(ct, dt_, self.n, budget.patterns, forced))
+                    continue
+                sig = scores(ct, dt_, self.n)
                 row.append(select(sig, forced, budget.mode, budget.density, budget.mass))
             result.append(row)
         return result

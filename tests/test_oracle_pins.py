@@ -321,6 +321,84 @@ def test_selection_ties_break_by_index():
     assert r.kept.tolist() == [0, 1, 2] and r.key_gap == 0.0
 
 
+# ------------------------------------------------------- pattern-level Top-K
+
+def _pattern_mask_bruteforce(c, d, n, K, forced):
+    """Kept blocks from explicit pattern sets: choose the K best patterns by
+    trying every K-subset of the 3n-1 patterns (values at float32, the
+    lexicographically smallest index set among equal sums), then mark the
+    blocks each chosen pattern covers from its definition."""
+    vals = [float(np.float32(x)) for x in list(c) + list(d)]
+    P = len(vals)
+    best = max(itertools.combinations(range(P), K),
+               key=lambda S: (sum(vals[p] for p in S), [-p for p in S]))
+    keep = forced.copy()
+    for p in best:
+        if p < 2 * n - 1:                      # diagonal delta = p - (n - 1)
+            delta = p - (n - 1)
+            for i in range(n):
+                if 0 <= i + delta < n:
+                    keep[i, i + delta] = True
+        else:                                  # column j
+            keep[:, p - (2 * n - 1)] = True
+    return keep
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_pattern_topk_bruteforce(seed):
+    rng = np.random.default_rng(300 + seed)
+    n = 4
+    c, d = rng.standard_normal(2 * n - 1), rng.standard_normal(n)
+    forced = np.zeros((n, n), bool)
+    if seed % 2:
+        forced[:2, :2] = forced[2:, 2:] = True
+    K = int(rng.integers(1, 3 * n))
+    got = O.select_patterns(c, d, n, K, forced)
+    want = _pattern_mask_bruteforce(c, d, n, K, forced)
+    for i in range(n):
+        assert got[i].kept.tolist() == np.flatnonzero(want[i]).tolist()
+
+
+def test_pattern_topk_planted_diagonal_and_column():
+    """Fit a map made of one parallel diagonal and one column: the two best
+    patterns of the minimum-norm fit are exactly those, and K = 2 keeps the
+    union of their blocks."""
+    n, bs = 16, 8
+    reg = O.frame_regions(n * bs, bs, n * bs // 2)
+    G = 0.02 * O.basis_C(n, -2) + 0.05 * O.basis_D(n, 5) + 0.001
+    c, d, _ = O.split_coeffs(O.fit(G, reg), n)
+    rows = O.select_patterns(c, d, n, 2, np.zeros((n, n), bool))
+    for i, r in enumerate(rows):
+        want = {5} | ({i - 2} if i >= 2 else set())
+        assert set(r.kept.tolist()) == want
+
+
+def test_pattern_topk_all_patterns_keep_every_block_and_ties():
+    n = 6
+    rows = O.select_patterns(np.zeros(2 * n - 1), np.zeros(n), n, 3 * n - 1, np.zeros((n, n), bool))
+    assert all(r.kept.tolist() == list(range(n)) for r in rows)
+    # equal intensities: the lowest pattern indices win (diagonals from the
+    # most negative offset, so K = 1 keeps block (n-1, 0) only)
+    rows = O.select_patterns(np.zeros(2 * n - 1), np.zeros(n), n, 1, np.zeros((n, n), bool))
+    assert [r.kept.tolist() for r in rows] == [[]] * (n - 1) + [[0]]
+    assert rows[0].key_gap == 0.0
+
+
+def test_pattern_topk_invariants():
+    rng = np.random.default_rng(7)
+    n = 12
+    c, d = rng.standard_normal(2 * n - 1), rng.standard_normal(n)
+    forced = O.forced_mask(n, [(0, 3), (3, 7), (8, 11)], True)
+    K = 9
+    rows = O.select_patterns(c, d, n, K, forced)
+    vals = np.concatenate([c, d]).astype(np.float32)
+    thr = np.sort(vals)[::-1][K - 1]
+    for i, r in enumerate(rows):
+        for j in range(n):
+            covered = vals[j - i + n - 1] >= thr or vals[2 * n - 1 + j] >= thr
+            assert (j in r.kept) == (covered or forced[i, j])
+
+
 # ---------------------------------------------------------------- a6 attention
 
 def test_full_mask_equals_textbook_attention():
