@@ -53,6 +53,7 @@ WORKLOADS = {
     "wan-720p-d10": ("wan", "topk", 0.10),
     "wan-720p-d05": ("wan", "topk", 0.05),
     "hunyuan-720p-dense": ("hunyuan", "topk", 1.0),
+    "hunyuan-720p-pattern": ("hunyuan", "pattern", 929),   # K = n patterns per head
     "small": ("small", "topk", 0.25),
 }
 WARMUP_M = 5          # dense warm-up steps before the timed sparse steps
@@ -214,7 +215,8 @@ def cpu_baseline(cfg, host, rows_h0, mode, val, total_flops, sample_rows):
     P.collect(q, k, WARMUP_M - 1)
     P.collect(q, k, WARMUP_M)
     budget = O.Budget(mode, density=val if mode == "topk" else 1.0,
-                      mass=val if mode == "mass" else 1.0)
+                      mass=val if mode == "mass" else 1.0,
+                      patterns=int(val) if mode == "pattern" else 1)
     n = P.n
     rows = [int(r) for r in np.linspace(0, n - 1, min(sample_rows, n)).round()]
     sizes = O.block_sizes(cfg.L, cfg.block)
@@ -457,7 +459,8 @@ def main():
     shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
     stats = M.Stats(shape, M.make_params(warmup_m=WARMUP_M, delta_t=1, tau_e=0.0, anchor_rule=0))
     n = stats.n
-    budget = M.make_budget(mode, density=val) if mode == "topk" else M.make_budget(mode, mass=val)
+    budget = (M.make_budget(mode, density=val) if mode == "topk" else
+              M.make_budget(mode, mass=val) if mode == "mass" else M.make_budget(mode, patterns=val))
     kv_idx = torch.empty((cfg.B, cfg.H, n, n), dtype=torch.int32, device=dev)
     kv_cnt = torch.empty((cfg.B, cfg.H, n), dtype=torch.int32, device=dev)
     out = torch.empty_like(qd)

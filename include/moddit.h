@@ -72,19 +72,28 @@ typedef struct {
                           (Algorithm 1)                                      */
 } mod_params;
 
-typedef enum { MOD_BUDGET_TOPK = 0, MOD_BUDGET_MASS = 1 } mod_budget_mode;
+typedef enum { MOD_BUDGET_TOPK = 0, MOD_BUDGET_MASS = 1, MOD_BUDGET_PATTERN = 2 } mod_budget_mode;
 
-/* Per-row sparsity budget.
+/* Sparsity budget.
  *   TOPK: keep k = clamp(ceil(density * n - 1e-6), 1, n) blocks per query
  *         block (density taken at float precision), the forced block-diagonal
  *         blocks counted first.
  *   MASS: keep the forced blocks plus the shortest score-ordered prefix of
  *         the others whose positive score mass reaches `mass` of the row's
- *         total positive mass (at least one block). */
+ *         total positive mass (at least one block).
+ *   PATTERN (Section 5.3, the mask as printed): per head, rank the 3n - 1
+ *         predicted intensities of the parallel-diagonal and vertical
+ *         patterns together (float precision, ties by pattern index:
+ *         diagonals j - i = -(n-1) .. n-1 first, then columns), keep the
+ *         `patterns` largest; block (i, j) is kept iff its diagonal or its
+ *         column is kept, or it is forced.  The ranking uses the
+ *         minimum-norm gauge of the fit.  A row that no kept pattern reaches
+ *         may be empty (its attention output is zero). */
 typedef struct {
-    int mode;          /* mod_budget_mode            */
-    float density;     /* TOPK: in (0, 1]            */
-    float mass;        /* MASS: in (0, 1]            */
+    int mode;          /* mod_budget_mode              */
+    float density;     /* TOPK: in (0, 1]              */
+    float mass;        /* MASS: in (0, 1]              */
+    int patterns;      /* PATTERN: K in [1, 3n - 1]    */
 } mod_budget;
 
 typedef struct mod_stats mod_stats;   /* opaque, library-owned */

@@ -25,6 +25,7 @@ MOD_ERR_HIP = 4
 MOD_ERR_NOMEM = 5
 MOD_BUDGET_TOPK = 0
 MOD_BUDGET_MASS = 1
+MOD_BUDGET_PATTERN = 2
 
 
 class ModError(RuntimeError):
@@ -44,7 +45,7 @@ class mod_params(ctypes.Structure):
 
 
 class mod_budget(ctypes.Structure):
-    _fields_ = [("mode", c_int), ("density", c_float), ("mass", c_float)]
+    _fields_ = [("mode", c_int), ("density", c_float), ("mass", c_float), ("patterns", c_int)]
 
 
 # torch bundles its own HIP runtime (SONAME libamdhip64.so.7).  Loading torch
@@ -129,9 +130,9 @@ def make_params(warmup_m=1, delta_t=0, tau_e=0.0, anchor_rule=0) -> mod_params:
     return mod_params(warmup_m, delta_t, tau_e, anchor_rule)
 
 
-def make_budget(mode="topk", density=1.0, mass=1.0) -> mod_budget:
-    m = {"topk": MOD_BUDGET_TOPK, "mass": MOD_BUDGET_MASS}.get(mode, mode)
-    return mod_budget(int(m), density, mass)
+def make_budget(mode="topk", density=1.0, mass=1.0, patterns=1) -> mod_budget:
+    m = {"topk": MOD_BUDGET_TOPK, "mass": MOD_BUDGET_MASS, "pattern": MOD_BUDGET_PATTERN}.get(mode, mode)
+    return mod_budget(int(m), density, mass, int(patterns))
 
 
 # ---------------------------------------------------------------- entry points

@@ -194,6 +194,7 @@ struct mod_stats {
     int* row_lo = nullptr;
     int* row_hi = nullptr;
     int32_t* gate = nullptr;
+    uint8_t* chosen = nullptr;   // pattern mode: chosen patterns [BH, 3n-1]
     // host state
     int n_anchors = 0;
     int newest = 1;            // slot of the newest anchor
@@ -210,7 +211,7 @@ namespace {
 void free_stats(mod_stats* s) {
     if (!s) return;
     void* ptrs[] = {s->qbar, s->kbar, s->G,   s->r,      s->bU,     s->u,   s->X[0], s->X[1],
-                    s->pred, s->Sinv, s->reg, s->row_lo, s->row_hi, s->gate};
+                    s->pred, s->Sinv, s->reg, s->row_lo, s->row_hi, s->gate, s->chosen};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     delete s;
@@ -323,6 +324,7 @@ mod_status mod_stats_create(const mod_shape* shape, const mod_params* params, mo
         {(void**)&s->row_lo, (size_t)n * sizeof(int)},
         {(void**)&s->row_hi, (size_t)n * sizeof(int)},
         {(void**)&s->gate, BH * sizeof(int32_t)},
+        {(void**)&s->chosen, BH * (3 * n - 1) * sizeof(uint8_t)},
     };
     for (auto& a : allocs) {
         hipError_t e = hipMalloc(a.p, a.bytes);
@@ -383,6 +385,9 @@ mod_status mod_predict_block_mask(mod_stats* s, const void* q, const void* k, in
         if (!(budget->mass > 0.0f && budget->mass <= 1.0f))
             return fail(MOD_ERR_INVALID_ARG, "MASS mass must be in (0, 1]");
         tau = (double)budget->mass;
+    } else if (budget->mode == MOD_BUDGET_PATTERN) {
+        if (budget->patterns < 1 || budget->patterns > 3 * n - 1)
+            return fail(MOD_ERR_INVALID_ARG, "PATTERN patterns must be in [1, 3n-1] = [1, %d]", 3 * n - 1);
     } else {
         return fail(MOD_ERR_INVALID_ARG, "unknown budget mode %d", budget->mode);
     }
@@ -415,8 +420,12 @@ mod_status mod_predict_block_mask(mod_stats* s, const void* q, const void* k, in
     }
     hipError_t e = moddit::launch_extrapolate(X1, X2, w, s->pred, s->BH, n, s->F, hs);
     if (e != hipSuccess) return hip_fail(e, "extrapolate launch");
-    e = moddit::launch_select(s->pred, s->gate, s->row_lo, s->row_hi, budget->mode, topk, tau, kv_idx,
-                              kv_cnt, s->BH, n, hs);
+    if (budget->mode == MOD_BUDGET_PATTERN)
+        e = moddit::launch_select_patterns(s->pred, s->gate, s->row_lo, s->row_hi, budget->patterns,
+                                           s->chosen, kv_idx, kv_cnt, s->BH, n, hs);
+    else
+        e = moddit::launch_select(s->pred, s->gate, s->row_lo, s->row_hi, budget->mode, topk, tau,
+                                  kv_idx, kv_cnt, s->BH, n, hs);
     if (e != hipSuccess) return hip_fail(e, "select launch");
     s->has_step = true;
     s->last_step = step;

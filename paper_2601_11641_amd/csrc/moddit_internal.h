@@ -42,6 +42,13 @@ hipError_t launch_select(const double* pred, const int32_t* gate, const int* row
                          const int* row_hi, int mode, int k, double tau, int32_t* kv_idx,
                          int32_t* kv_cnt, int BH, int n, hipStream_t s);
 
+// a5, pattern form: the K largest pattern intensities per head (chosen
+// [BH, 3n-1] bytes, scratch), then per-row lists of the blocks a chosen
+// diagonal or column covers, plus the forced blocks.
+hipError_t launch_select_patterns(const double* pred, const int32_t* gate, const int* row_lo,
+                                  const int* row_hi, int K, uint8_t* chosen, int32_t* kv_idx,
+                                  int32_t* kv_cnt, int BH, int n, hipStream_t s);
+
 // a6: block-sparse attention forward.
 hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                            const int32_t* kv_idx, const int32_t* kv_cnt, float scale,

@@ -503,6 +503,104 @@ inline unsigned cdiv(long a, long b) { return static_cast<unsigned>((a + b - 1) 
 
 }  // namespace
 
+// ---------------------------------------------------------------------------
+// a5, pattern form (Section 5.3): per head, the K largest of the 3n - 1
+// predicted pattern intensities (diagonals delta = -(n-1)..n-1 at index
+// delta + n - 1, then columns j at 2n - 1 + j), keys at float32 precision,
+// ties by pattern index.  The 64-bit key (order_bits(value) << 32 | ~index)
+// is unique, so the K-th largest key is found exactly by an 8-pass radix
+// select over 8-bit digits; a pattern is chosen iff its key reaches it.
+// Then per row, block (i, j) is kept iff its diagonal or its column is
+// chosen or it is forced; the kept blocks are compacted in ascending j.
+// ---------------------------------------------------------------------------
+__device__ inline uint64_t pattern_key(const double* v, int p) {
+    return (static_cast<uint64_t>(order_bits(static_cast<float>(v[p]))) << 32) |
+           static_cast<uint64_t>(0xFFFFFFFFu - static_cast<uint32_t>(p));
+}
+
+__global__ __launch_bounds__(kThreads) void pattern_rank_kernel(const double* __restrict__ pred,
+                                                                 uint8_t* __restrict__ chosen,
+                                                                 int n, int K) {
+    __shared__ uint32_t hist[256];
+    __shared__ uint64_t s_prefix;
+    __shared__ int s_need;
+    const int P = 3 * n - 1;
+    const int bh = blockIdx.x, t = threadIdx.x;
+    const double* v = pred + (size_t)bh * P;
+    if (t == 0) {
+        s_prefix = 0;
+        s_need = K;
+    }
+    for (int pass = 0; pass < 8; ++pass) {
+        const int shift = 56 - 8 * pass;
+        const uint64_t hi_mask = pass == 0 ? 0ull : (~0ull << (shift + 8));
+        hist[t] = 0;      // kThreads == 256 bins
+        __syncthreads();
+        const uint64_t prefix = s_prefix;
+        for (int q = t; q < P; q += kThreads) {
+            const uint64_t key = pattern_key(v, q);
+            if ((key & hi_mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+        }
+        __syncthreads();
+        if (t == 0) {
+            int need = s_need;
+            uint32_t cum = 0;
+            for (int dgt = 255; dgt >= 0; --dgt) {
+                if (cum + hist[dgt] >= (uint32_t)need) {
+                    s_prefix = prefix | (static_cast<uint64_t>(dgt) << shift);
+                    s_need = need - (int)cum;
+                    break;
+                }
+                cum += hist[dgt];
+            }
+        }
+        __syncthreads();
+    }
+    const uint64_t kth = s_prefix;    // the K-th largest key (keys are unique)
+    for (int q = t; q < P; q += kThreads) chosen[(size_t)bh * P + q] = pattern_key(v, q) >= kth ? 1 : 0;
+}
+
+__global__ __launch_bounds__(kThreads) void pattern_rows_kernel(
+    const uint8_t* __restrict__ chosen, const int32_t* __restrict__ gate,
+    const int* __restrict__ row_lo, const int* __restrict__ row_hi, int32_t* __restrict__ kv_idx,
+    int32_t* __restrict__ kv_cnt, int n) {
+    __shared__ int wtot[kThreads / 64];
+    constexpr int JPT = kMaxBlocks / kThreads;
+    const int row = blockIdx.x;
+    const int bh = row / n, i = row % n;
+    const uint8_t* ch = chosen + (size_t)bh * (3 * n - 1);
+    const bool g = gate[bh] != 0;
+    const int flo = row_lo[i], fhi = row_hi[i];
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    bool keep[JPT];
+    int mine = 0;
+#pragma unroll
+    for (int e = 0; e < JPT; ++e) {
+        const int j = t * JPT + e;
+        keep[e] = j < n && (ch[j - i + n - 1] || ch[2 * n - 1 + j] || (g && j >= flo && j <= fhi));
+        mine += keep[e] ? 1 : 0;
+    }
+    int incl = mine;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(incl, off);
+        if (lane >= off) incl += y;
+    }
+    if (lane == 63) wtot[w] = incl;
+    __syncthreads();
+    int pos = incl - mine, total = 0;
+#pragma unroll
+    for (int ww = 0; ww < kThreads / 64; ++ww) {
+        pos += ww < w ? wtot[ww] : 0;
+        total += wtot[ww];
+    }
+    int32_t* out = kv_idx + (size_t)row * n;
+#pragma unroll
+    for (int e = 0; e < JPT; ++e)
+        if (keep[e]) out[pos++] = t * JPT + e;
+    if (t == 0) kv_cnt[row] = total;
+}
+
 hipError_t launch_pool(const uint16_t* q, const uint16_t* k, double* qbar, double* kbar,
                        int BH, int L, int d, int bs, int n, hipStream_t s) {
     const dim3 grid(n, BH, 2);
@@ -581,6 +679,17 @@ hipError_t launch_select(const double* pred, const int32_t* gate, const int* row
     }
     hipLaunchKernelGGL(select_kernel, dim3((unsigned)BH * n), dim3(kThreads), lds, s, pred, gate,
                        row_lo, row_hi, mode, k, tau, kv_idx, kv_cnt, n, npad);
+    return hipGetLastError();
+}
+
+hipError_t launch_select_patterns(const double* pred, const int32_t* gate, const int* row_lo,
+                                  const int* row_hi, int K, uint8_t* chosen, int32_t* kv_idx,
+                                  int32_t* kv_cnt, int BH, int n, hipStream_t s) {
+    hipLaunchKernelGGL(pattern_rank_kernel, dim3((unsigned)BH), dim3(kThreads), 0, s, pred, chosen, n, K);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(pattern_rows_kernel, dim3((unsigned)BH * n), dim3(kThreads), 0, s, chosen, gate,
+                       row_lo, row_hi, kv_idx, kv_cnt, n);
     return hipGetLastError();
 }
 

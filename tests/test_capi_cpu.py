@@ -87,3 +87,32 @@ def test_attention_rejects_null_pointers_on_host(M):
 
 def test_workspace_size(M):
     assert M.mod_attn_workspace_bytes(M.make_shape(1, 24, 118800, 128, 128, 3600)) >= 0
+
+
+def test_struct_layouts_match_the_header(M, tmp_path):
+    """The ctypes mirrors of the ABI structs have the header's layout
+    (sizes and field offsets from a C program compiled against it)."""
+    import ctypes
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "layout.c"
+    src.write_text(
+        '#include <stddef.h>\n#include <stdio.h>\n#include "moddit.h"\n'
+        'int main(void) {\n'
+        '  printf("%zu %zu %zu %zu %zu\\n", sizeof(mod_budget), offsetof(mod_budget, mode),\n'
+        '         offsetof(mod_budget, density), offsetof(mod_budget, mass), offsetof(mod_budget, patterns));\n'
+        '  printf("%zu %zu\\n", sizeof(mod_shape), offsetof(mod_shape, frame_tokens));\n'
+        '  printf("%zu %zu\\n", sizeof(mod_params), offsetof(mod_params, anchor_rule));\n'
+        '  return 0;\n}\n')
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split()
+    got = [int(x) for x in out]
+    want = [ctypes.sizeof(M.mod_budget), M.mod_budget.mode.offset, M.mod_budget.density.offset,
+            M.mod_budget.mass.offset, M.mod_budget.patterns.offset,
+            ctypes.sizeof(M.mod_shape), M.mod_shape.frame_tokens.offset,
+            ctypes.sizeof(M.mod_params), M.mod_params.anchor_rule.offset]
+    assert got == want

@@ -12,7 +12,7 @@ import oracle as O
 import paper_2601_11641_amd as M
 import workloads as W
 from parity import (LSE_ABS, MAX_ABS, MEAN_ABS, attention_errors, bf16_tensor, bf16_to_f64,
-                    compare_lists, gpu_lists)
+                    compare_lists, compare_pattern_head, gpu_lists)
 
 torch = pytest.importorskip("torch")
 pytestmark = [pytest.mark.gpu,
@@ -48,7 +48,8 @@ def _gpu_predict(cfg, dev, budget):
     idx = torch.empty((cfg.B, cfg.H, n, n), dtype=torch.int32, device="cuda")
     cnt = torch.empty((cfg.B, cfg.H, n), dtype=torch.int32, device="cuda")
     mode, val = budget
-    gb = M.make_budget(mode, density=val) if mode == "topk" else M.make_budget(mode, mass=val)
+    gb = (M.make_budget(mode, density=val) if mode == "topk" else
+          M.make_budget(mode, mass=val) if mode == "mass" else M.make_budget(mode, patterns=val))
     M.mod_predict_block_mask(st.handle, qd, kd, WARM + 1, gb, idx, cnt)
     torch.cuda.synchronize()
     return st, idx, cnt
@@ -65,7 +66,8 @@ def _check_heads(cfg, host, st, idx, cnt, budget, heads):
     P.collect(qf, kf, WARM)
     mode, val = budget
     sel = P.predict(qf, kf, WARM + 1, O.Budget(mode, density=val if mode == "topk" else 1.0,
-                                               mass=val if mode == "mass" else 1.0))
+                                               mass=val if mode == "mass" else 1.0,
+                                               patterns=val if mode == "pattern" else 1))
     n = st.n
     X, _ = M.mod_stats_get_anchor(st.handle, 0, cfg.B, cfg.H, st.p)
     Xo = P.anchors[-1][1]
@@ -77,6 +79,11 @@ def _check_heads(cfg, host, st, idx, cnt, budget, heads):
     for hi, h in enumerate(heads):
         assert np.abs(X[0, h] - Xo[0, hi]).max() <= 1e-9 * max(1.0, np.abs(Xo[0, hi]).max())
         assert bool(gate[0, h]) == bool(P.gates[0, hi])
+        if mode == "pattern":
+            nr, _, xh, bad = compare_pattern_head(rows[0][h], sel[0][hi], n)
+            assert not bad, f"head {h}: rows {bad[:10]} differ"
+            total, excused = total + nr, excused + (nr if xh else 0)
+            continue
         ct, dt_ = P.prediction(WARM + 1)[0][hi]
         sig = O.scores(ct, dt_, n)
         forced = O.forced_mask(n, P.regions, bool(P.gates[0, hi]))
@@ -125,6 +132,18 @@ def test_720p_mass_budget(layer):
 def test_720p_topk_densities(layer, density):
     cfg, host, dev = layer
     budget = ("topk", density)
+    st, idx, cnt = _gpu_predict(cfg, dev, budget)
+    heads = _sample_heads(cfg)[::2]
+    _check_heads(cfg, host, st, idx, cnt, budget, heads)
+    _check_attention_rows(cfg, host, dev, idx, cnt, heads, nrows=3)
+    st.close()
+
+
+@pytest.mark.parametrize("per_n", [0.5, 2.0])
+def test_720p_pattern_mode(layer, per_n):
+    """Pattern-level Top-K with K = per_n * n patterns per head."""
+    cfg, host, dev = layer
+    budget = ("pattern", int(per_n * cfg.n))
     st, idx, cnt = _gpu_predict(cfg, dev, budget)
     heads = _sample_heads(cfg)[::2]
     _check_heads(cfg, host, st, idx, cnt, budget, heads)

@@ -13,7 +13,7 @@ import pytest
 import oracle as O
 import workloads as W
 from parity import (GAP, LSE_ABS, MAX_ABS, MEAN_ABS, attention_errors, bf16_tensor, bf16_to_f64,
-                    compare_lists, gpu_lists)
+                    compare_lists, compare_pattern_head, gpu_lists)
 
 import paper_2601_11641_amd as M
 
@@ -47,6 +47,17 @@ def _inputs(cfg):
     return (q, k, v), tuple(bf16_tensor(x) for x in (q, k, v))
 
 
+def _budgets(budget):
+    """(C-ABI budget, oracle budget) for ("topk", rho), ("mass", tau) or
+    ("pattern", K)."""
+    mode, val = budget
+    if mode == "topk":
+        return M.make_budget(mode, density=val), O.Budget(mode, density=val)
+    if mode == "mass":
+        return M.make_budget(mode, mass=val), O.Budget(mode, mass=val)
+    return M.make_budget(mode, patterns=val), O.Budget(mode, patterns=val)
+
+
 def _run_predictor(cfg, dev, host, warm, step, budget, params):
     qd, kd, _ = dev
     shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
@@ -56,8 +67,7 @@ def _run_predictor(cfg, dev, host, warm, step, budget, params):
     n = st.n
     kv_idx = torch.full((cfg.B, cfg.H, n, n), -1, dtype=torch.int32, device="cuda")
     kv_cnt = torch.zeros((cfg.B, cfg.H, n), dtype=torch.int32, device="cuda")
-    mode, val = budget
-    gb = M.make_budget(mode, density=val) if mode == "topk" else M.make_budget(mode, mass=val)
+    gb, ob = _budgets(budget)
     M.mod_predict_block_mask(st.handle, qd, kd, step, gb, kv_idx, kv_cnt)
     torch.cuda.synchronize()
 
@@ -65,8 +75,6 @@ def _run_predictor(cfg, dev, host, warm, step, budget, params):
     P = O.Predictor(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens, **params)
     for t in warm:
         P.collect(qf, kf, t)
-    mode, val = budget
-    ob = O.Budget(mode, density=val if mode == "topk" else 1.0, mass=val if mode == "mass" else 1.0)
     sel = P.predict(qf, kf, step, ob)
     return st, kv_idx, kv_cnt, P, sel, qf, kf
 
@@ -98,6 +106,15 @@ def _check_predictor(cfg, st, kv_idx, kv_cnt, P, sel, qf, kf, budget, step):
     k = O.topk_count(val, n) if mode == "topk" else 0
     tau = val if mode == "mass" else 1.0
     total = exact = excused = 0
+    if mode == "pattern":
+        heads_excused = 0
+        for b in range(B):
+            for h in range(H):
+                nr, ne, xh, bad = compare_pattern_head(rows[b][h], sel[b][h], n)
+                assert not bad, f"head ({b},{h}) rows {bad[:10]} differ"
+                heads_excused += int(xh)
+        assert heads_excused <= max(1, 0.05 * B * H), heads_excused
+        return rows
     for b in range(B):
         for h in range(H):
             ct, dt_ = po[b][h]
@@ -200,6 +217,45 @@ def test_ragged_shapes(name, budget):
     st.close()
 
 
+@pytest.mark.parametrize("K", [1, 5, 12, 47])
+def test_tiny_pattern_mode(K):
+    """Pattern-level Top-K (K of the 3n-1 = 47 patterns; 47 keeps all)."""
+    cfg = W.CONFIGS["tiny"]
+    host, dev = _inputs(cfg)
+    params = dict(warmup_m=1, delta_t=0)
+    budget = ("pattern", K)
+    st, kv_idx, kv_cnt, P, sel, qf, kf = _run_predictor(cfg, dev, host, [1], 2, budget, params)
+    rows = _check_predictor(cfg, st, kv_idx, kv_cnt, P, sel, qf, kf, budget, 2)
+    if K == 3 * st.n - 1:
+        assert all(r == list(range(st.n)) for hh in rows[0] for r in hh)
+    _check_attention(cfg, dev, host, rows)
+    st.close()
+
+
+@pytest.mark.parametrize("K", [32, 128])
+def test_small_pattern_mode(K):
+    cfg = W.CONFIGS["small"]
+    host, dev = _inputs(cfg)
+    params = dict(warmup_m=5, delta_t=10)
+    budget = ("pattern", K)
+    st, kv_idx, kv_cnt, P, sel, qf, kf = _run_predictor(cfg, dev, host, [4, 5], 6, budget, params)
+    rows = _check_predictor(cfg, st, kv_idx, kv_cnt, P, sel, qf, kf, budget, 6)
+    _check_attention(cfg, dev, host, rows)
+    st.close()
+
+
+@pytest.mark.parametrize("name", sorted(RAGGED))
+def test_ragged_pattern_mode(name):
+    cfg = RAGGED[name]
+    host, dev = _inputs(cfg)
+    params = dict(warmup_m=2, delta_t=0, tau_e=-1.0)   # gate on: forced blocks too
+    budget = ("pattern", cfg.n)
+    st, kv_idx, kv_cnt, P, sel, qf, kf = _run_predictor(cfg, dev, host, [1, 2], 4, budget, params)
+    rows = _check_predictor(cfg, st, kv_idx, kv_cnt, P, sel, qf, kf, budget, 4)
+    _check_attention(cfg, dev, host, rows)
+    st.close()
+
+
 def test_attention_empty_and_single_rows():
     """Rows with no kept block give O = 0 and lse = -inf; single-block rows
     match the oracle."""
@@ -231,6 +287,10 @@ def test_state_errors_on_device():
     with pytest.raises(M.ModError) as e:
         M.mod_predict_block_mask(st.handle, qd, kd, 3, M.make_budget("topk", 0.0), idx, cnt)
     assert e.value.status == M.MOD_ERR_INVALID_ARG
+    for K in (0, 3 * n):
+        with pytest.raises(M.ModError) as e:
+            M.mod_predict_block_mask(st.handle, qd, kd, 3, M.make_budget("pattern", patterns=K), idx, cnt)
+        assert e.value.status == M.MOD_ERR_INVALID_ARG
     with pytest.raises(M.ModError) as e:   # step 5 = m + dt re-anchors: q, k needed
         M.mod_predict_block_mask(st.handle, None, None, 5, M.make_budget("topk", 0.5), idx, cnt)
     assert e.value.status == M.MOD_ERR_INVALID_ARG
