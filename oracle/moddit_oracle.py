@@ -487,11 +487,16 @@ class Predictor:
     rule 1 uses t mod dt == 0 (Algorithm 1).  dt <= 0 never re-anchors.
     The block-diagonal gate is fixed at the first predict from the anchors
     held then (the warm-up anchors m-1, m).
+    statistic="attention" fits the Eq. 2 statistic of the attention a step
+    computed instead of the pooled block mass: update(q, k, kept, t) after
+    the attention of a dense warm-up step or a re-anchor step (Eq. 5 keeps
+    the dropped blocks at their history); predict() then never re-anchors
+    by itself.
     q, k: fp64 [B, H, L, d].
     """
 
     def __init__(self, B, H, L, d, bs, frame_tokens, warmup_m, delta_t, tau_e=0.0,
-                 anchor_rule=0, scale=None):
+                 anchor_rule=0, scale=None, statistic="pooled", eta=1e-4):
         self.B, self.H, self.L, self.d, self.bs = B, H, L, d, bs
         self.n = num_blocks(L, bs)
         self.regions = frame_regions(L, bs, frame_tokens)
@@ -503,6 +508,8 @@ class Predictor:
         self.last_step = None
         self.gates = None          # bool [B, H]
         self._N = normal_matrix(self.n, self.regions)
+        self.statistic, self.eta = statistic, eta
+        self.stat = None           # "attention": reconstructed map [B, H, n, n]
 
     def is_anchor_step(self, t: int) -> bool:
         if self.dt <= 0:
@@ -529,9 +536,42 @@ class Predictor:
         self.last_step = t
 
     def collect(self, q, k, t):
+        if self.statistic != "pooled":
+            raise ValueError("collect() is the pooled statistic's entry; use update()")
         self._advance(t)
         self.anchors.append((t, self.fit_all(q, k)))
         self.anchors = self.anchors[-2:]
+
+    def fit_map(self, Smap) -> np.ndarray:
+        X = np.empty((self.B, self.H, num_coeffs(self.n, self.F)))
+        for b in range(self.B):
+            for h in range(self.H):
+                X[b, h] = solve_min_norm(self._N, rhs(Smap[b, h], self.regions), self.n, self.F)
+        return X
+
+    def update_from_statistic(self, current, t):
+        """Anchor at step t from the statistic of the blocks the step kept
+        (current [B, H, n, n], NaN where not kept): Eq. 5 reconstruction,
+        then the least-squares fit."""
+        self._advance(t)
+        self.stat = np.stack([np.stack([reconstruct_statistic(
+            None if self.stat is None else self.stat[b, h], current[b, h])
+            for h in range(self.H)]) for b in range(self.B)])
+        self.anchors.append((t, self.fit_map(self.stat)))
+        self.anchors = self.anchors[-2:]
+
+    def update(self, q, k, kept, t, lse=None):
+        """Attention statistic (Eq. 2) of step t's attention over the kept
+        blocks (kept[b][h][i]: lists; full lists at a dense step), then
+        update_from_statistic.  lse: optional [B, H, L] row LSE."""
+        if self.statistic != "attention":
+            raise ValueError("update() needs statistic='attention'")
+        cur = np.empty((self.B, self.H, self.n, self.n))
+        for b in range(self.B):
+            for h in range(self.H):
+                cur[b, h] = attention_statistic(q[b, h], k[b, h], kept[b][h], self.bs, self.scale,
+                                                self.eta, None if lse is None else lse[b, h])[0]
+        self.update_from_statistic(cur, t)
 
     def prediction(self, t):
         """(c~, d~) per (b, h) at step t from the anchors held."""
@@ -554,7 +594,7 @@ class Predictor:
             self.gates = np.array([[gate([split_coeffs(X[b, h], self.n)[2]
                                           for _, X in self.anchors], self.tau_e)
                                     for h in range(self.H)] for b in range(self.B)])
-        if self.is_anchor_step(t):
+        if self.statistic == "pooled" and self.is_anchor_step(t):
             self.anchors.append((t, self.fit_all(q, k)))
             self.anchors = self.anchors[-2:]
         pred = self.prediction(t)
@@ -571,6 +611,70 @@ class Predictor:
                 row.append(select(sig, forced, budget.mode, budget.density, budget.mass))
             result.append(row)
         return result
+
+
+# ----------------------------------------------------------------------------
+# Eq. 2 / Eq. 5: the attention sparsity statistic of the paper
+# ----------------------------------------------------------------------------
+
+
+def attention_statistic(q: np.ndarray, k: np.ndarray, kept_lists, bs: int, scale: float,
+                        eta: float, lse: np.ndarray | None = None, tol: float = 0.0):
+    """Eq. 2 on the attention map a step computed: for every kept block
+    (i, j), the fraction of its probabilities A(p, q) = exp(scale q_p.k_q -
+    LSE_p) that reach eta, where LSE_p normalises over the kept blocks of
+    row block i (the masked map of Section 4.1; all blocks at a dense step).
+    This is 1 - S(i, j), the informativeness the MOD model is fitted to
+    (reading: larger = kept; the fraction is over the block's valid entries,
+    so a short tail block is not padded with "sparse" entries).
+
+    q, k: [L, d] fp64 of one head.  lse: optional [L] row LSE to compare
+    against (default: the exact masked LSE).  Returns (I, amb): I [n, n]
+    with NaN for blocks not kept; amb [n, n] the number of entries whose
+    log-probability lies within tol of log(eta) (where two implementations
+    may round the decision differently).
+    """
+    L = q.shape[0]
+    n = num_blocks(L, bs)
+    I = np.full((n, n), np.nan)
+    amb = np.zeros((n, n), dtype=np.int64)
+    log_eta = math.log(eta)
+    for i in range(n):
+        blocks = list(kept_lists[i])
+        if not blocks:
+            continue
+        qs = slice(i * bs, min(L, (i + 1) * bs))
+        idx = np.concatenate([np.arange(j * bs, min(L, (j + 1) * bs)) for j in blocks])
+        a = scale * (q[qs] @ k[idx].T)
+        if lse is None:
+            mx = a.max(axis=1, keepdims=True)
+            row_lse = mx + np.log(np.exp(a - mx).sum(axis=1, keepdims=True))
+        else:
+            row_lse = lse[qs][:, None]
+        logp = a - row_lse
+        start = 0
+        for j in blocks:
+            w = min(L, (j + 1) * bs) - j * bs
+            blk = logp[:, start:start + w]
+            start += w
+            I[i, j] = float((blk >= log_eta).sum()) / blk.size
+            amb[i, j] = int((np.abs(blk - log_eta) < tol).sum())
+    return I, amb
+
+
+def reconstruct_statistic(history: np.ndarray | None, current: np.ndarray) -> np.ndarray:
+    """Eq. 5 at block level: entries computed at this step (finite in
+    ``current``) replace the history; blocks the mask dropped keep their
+    historical value.  The first map must be dense (Algorithm 1 starts the
+    sequence from the full attention of the warm-up)."""
+    if history is None:
+        if np.isnan(current).any():
+            raise ValueError("the first statistic must cover every block (dense step)")
+        return current.copy()
+    out = history.copy()
+    kept = ~np.isnan(current)
+    out[kept] = current[kept]
+    return out
 
 
 # ----------------------------------------------------------------------------

@@ -399,6 +399,85 @@ def test_pattern_topk_invariants():
             assert (j in r.kept) == (covered or forced[i, j])
 
 
+# ------------------------------------------- Eq. 2 / Eq. 5 attention statistic
+
+@pytest.mark.parametrize("seed", range(3))
+def test_attention_statistic_bruteforce(seed):
+    """Fractions of softmax probabilities >= eta per kept block, against a
+    library softmax over the kept tokens and explicit per-entry counting."""
+    rng = np.random.default_rng(400 + seed)
+    L, d, bs, scale, eta = 150, 8, 32, 0.4, 3e-3
+    q, k = rng.standard_normal((L, d)), rng.standard_normal((L, d))
+    n = O.num_blocks(L, bs)
+    kept = [sorted(rng.choice(n, size=int(rng.integers(1, n + 1)), replace=False).tolist())
+            for _ in range(n)]
+    I, _ = O.attention_statistic(q, k, kept, bs, scale, eta)
+    for i in range(n):
+        rows = range(i * bs, min(L, (i + 1) * bs))
+        cols = [c for j in kept[i] for c in range(j * bs, min(L, (j + 1) * bs))]
+        for p in rows:
+            pr = scipy.special.softmax(scale * np.array([q[p] @ k[c] for c in cols]))
+            if p == rows[0]:
+                counts = {j: 0 for j in kept[i]}
+            for c, v in zip(cols, pr):
+                if v >= eta:
+                    counts[c // bs] += 1
+        for j in range(n):
+            if j in kept[i]:
+                size = (min(L, (i + 1) * bs) - i * bs) * (min(L, (j + 1) * bs) - j * bs)
+                assert I[i, j] == counts[j] / size
+            else:
+                assert np.isnan(I[i, j])
+
+
+def test_attention_statistic_uniform_attention_closed_form():
+    """q = 0 gives uniform attention 1/m over the m kept tokens of a row:
+    eta = 1/m counts every entry, eta slightly above counts none; eta -> 0
+    counts all, eta > 1 none."""
+    rng = np.random.default_rng(1)
+    L, d, bs = 96, 4, 32
+    q, k = np.zeros((L, d)), rng.standard_normal((L, d))
+    kept = [[0, 2], [1], [0, 1, 2]]
+    for i, js in enumerate(kept):
+        m = 32 * len(js)
+        for eta, want in ((1.0 / m, 1.0), (1.0 / m * (1 + 1e-9), 0.0), (1e-300, 1.0), (1.5, 0.0)):
+            I, _ = O.attention_statistic(q, k, kept, bs, 1.0, eta)
+            assert all(I[i, j] == want for j in js)
+
+
+def test_reconstruction_keeps_dropped_blocks():
+    rng = np.random.default_rng(2)
+    hist = rng.random((5, 5))
+    cur = np.full((5, 5), np.nan)
+    cur[1, 2], cur[4, 0] = 0.25, 0.75
+    out = O.reconstruct_statistic(hist, cur)
+    mask = np.zeros((5, 5), bool)
+    mask[1, 2] = mask[4, 0] = True
+    assert (out[~mask] == hist[~mask]).all() and out[1, 2] == 0.25 and out[4, 0] == 0.75
+    with pytest.raises(ValueError):
+        O.reconstruct_statistic(None, cur)
+
+
+def test_attention_predictor_dense_anchor_equals_lstsq_of_dense_map():
+    """Two dense warm-up updates: the anchors are the minimum-norm least
+    squares fits (library lstsq) of 1 - S of Eq. 2 on the dense maps."""
+    rng = np.random.default_rng(3)
+    B, H, L, d, bs, tf = 1, 2, 256, 8, 32, 64
+    q, k = rng.standard_normal((B, H, L, d)), rng.standard_normal((B, H, L, d))
+    P = O.Predictor(B, H, L, d, bs, tf, warmup_m=2, delta_t=0, statistic="attention", eta=2e-3)
+    n = P.n
+    full = [[[list(range(n))] * n for _ in range(H)] for _ in range(B)]
+    P.update(q, k, full, 1)
+    P.update(q * 0.9, k, full, 2)
+    for h in range(H):
+        S = O.sparsity_map(q[0, h] * 0.9, k[0, h], bs, P.scale, 2e-3)
+        Msys = O.design_matrix(n, P.regions)
+        X, *_ = np.linalg.lstsq(Msys, (1.0 - S).reshape(-1), rcond=None)
+        np.testing.assert_allclose(P.anchors[-1][1][0, h], X, atol=1e-10)
+    sel = P.predict(None, None, 3, O.Budget("topk", density=0.5))
+    assert all(len(r.kept) == O.topk_count(0.5, n) for r in sel[0][0])
+
+
 # ---------------------------------------------------------------- a6 attention
 
 def test_full_mask_equals_textbook_attention():
