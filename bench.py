@@ -331,7 +331,10 @@ def run_schedule(args):
     lists) with statistics collected at steps 4 and 5, steps 6-50 predicted
     masks (mass 0.75) + block-sparse attention; inputs drift between two draws
     (seeds 1005, 1006) as Q_t = cos(theta_t) Q0 + sin(theta_t) Q1 (same for K).
-    Run for re-anchor intervals 10 and 1."""
+    Run with the pooled statistic at re-anchor intervals 10 and 1, and with
+    the attention statistic of Eq. 2 / Eq. 5 at interval 10 (its re-anchor
+    update runs after the step's attention and is counted as predictor
+    time)."""
     import numpy as np
     import torch
 
@@ -362,8 +365,10 @@ def run_schedule(args):
         return ((c * q0.float() + s_ * q1.float()).to(torch.bfloat16),
                 (c * k0.float() + s_ * k1.float()).to(torch.bfloat16))
 
-    for dt in (10, 1):
-        st = M.Stats(shape, M.make_params(warmup_m=WARMUP_M, delta_t=dt))
+    lse = torch.empty((cfg.B, cfg.H, cfg.L), dtype=torch.float32, device=dev)
+    for statistic, dt in (("pooled", 10), ("pooled", 1), ("attention", 10)):
+        st = M.Stats(shape, M.make_params(warmup_m=WARMUP_M, delta_t=dt, statistic=statistic))
+        attn_stat = statistic == "attention"
         kv_idx = torch.empty((cfg.B, cfg.H, n, n), dtype=torch.int32, device=dev)
         kv_cnt = torch.empty((cfg.B, cfg.H, n), dtype=torch.int32, device=dev)
         dense_ms, sparse_ms, pred_anchor, pred_other, collect_ms, dens = [], [], [], [], [], []
@@ -373,11 +378,14 @@ def run_schedule(args):
             e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
             if t <= WARMUP_M:
                 e[0].record(stream)
-                M.mod_block_sparse_attn_fwd(shape, qt, kt, v0, full_idx, full_cnt, 0.0, out, None, None, 0,
-                                            stream)
+                M.mod_block_sparse_attn_fwd(shape, qt, kt, v0, full_idx, full_cnt, 0.0, out,
+                                            lse if attn_stat else None, None, 0, stream)
                 e[1].record(stream)
                 if t >= WARMUP_M - 1:
-                    M.mod_collect_stats(st.handle, qt, kt, t, stream)
+                    if attn_stat:
+                        M.mod_update_stats(st.handle, qt, kt, lse, full_idx, full_cnt, t, stream)
+                    else:
+                        M.mod_collect_stats(st.handle, qt, kt, t, stream)
                 e[2].record(stream)
                 torch.cuda.synchronize()
                 dense_ms.append(e[0].elapsed_time(e[1]))
@@ -385,13 +393,19 @@ def run_schedule(args):
                     collect_ms.append(e[1].elapsed_time(e[2]))
             else:
                 anchor = (t - WARMUP_M) % dt == 0
+                e.append(torch.cuda.Event(enable_timing=True))
                 e[0].record(stream)
                 M.mod_predict_block_mask(st.handle, qt, kt, t, budget, kv_idx, kv_cnt, stream)
                 e[1].record(stream)
-                M.mod_block_sparse_attn_fwd(shape, qt, kt, v0, kv_idx, kv_cnt, 0.0, out, None, None, 0, stream)
+                M.mod_block_sparse_attn_fwd(shape, qt, kt, v0, kv_idx, kv_cnt, 0.0, out,
+                                            lse if (attn_stat and anchor) else None, None, 0, stream)
                 e[2].record(stream)
+                if attn_stat and anchor:      # re-anchor from this step's attention (Eq. 5)
+                    M.mod_update_stats(st.handle, qt, kt, lse, kv_idx, kv_cnt, t, stream)
+                e[3].record(stream)
                 torch.cuda.synchronize()
-                (pred_anchor if anchor else pred_other).append(e[0].elapsed_time(e[1]))
+                (pred_anchor if anchor else pred_other).append(e[0].elapsed_time(e[1])
+                                                              + e[2].elapsed_time(e[3]))
                 sparse_ms.append(e[1].elapsed_time(e[2]))
                 dens.append(kept_flops(kv_idx, kv_cnt, cfg.L, cfg.block, cfg.d)
                             / (4.0 * cfg.d * cfg.L * cfg.L * cfg.B * cfg.H))
@@ -400,7 +414,7 @@ def run_schedule(args):
         total_pred = sum(pred_anchor) + sum(pred_other) + sum(collect_ms)
         print(json.dumps({
             "workload": "hunyuan-720p 50-step schedule (B=1 H=24 L=118800 d=128 block=128), mass 0.75",
-            "delta_t": dt, "steps": T, "dense_steps": WARMUP_M,
+            "statistic": statistic, "delta_t": dt, "steps": T, "dense_steps": WARMUP_M,
             "dense_attn_ms_avg": round(float(np.mean(dense_ms)), 3),
             "sparse_attn_ms_avg": round(float(np.mean(sparse_ms)), 3),
             "kept_density_avg": round(float(np.mean(dens)), 4),

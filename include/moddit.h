@@ -16,6 +16,9 @@
  *                            extrapolate c and d (Section 5.2), score blocks and
  *                            select per query block (Section 5.3)
  *   mod_block_sparse_attn_fwd  softmax attention over the kept blocks (Eq. 1)
+ *   mod_update_stats         (statistic 1) after a step's attention: the
+ *                            sparsity statistic of Eq. 2 on the blocks it
+ *                            computed, reconstruction of Eq. 5, fit
  *
  * Conventions shared by every entry point
  *   - Q, K, V, O are bfloat16, contiguous [B, H, L, d] (d fastest), device
@@ -70,6 +73,13 @@ typedef struct {
     int anchor_rule;   /* 0: re-anchor at t = m + i*delta_t, i >= 1 (the
                           prediction steps of Section 5); 1: at t % delta_t == 0
                           (Algorithm 1)                                      */
+    int statistic;     /* 0: the pooled block-mass statistic, fitted from Q, K
+                          (mod_collect_stats, and inside mod_predict_block_mask
+                          at re-anchor steps); 1: the attention sparsity
+                          statistic of Eq. 2 with the reconstruction of Eq. 5,
+                          fitted from the attention a step computed
+                          (mod_update_stats only)                            */
+    float eta;         /* statistic 1: sparsity threshold of Eq. 2, > 0     */
 } mod_params;
 
 typedef enum { MOD_BUDGET_TOPK = 0, MOD_BUDGET_MASS = 1, MOD_BUDGET_PATTERN = 2 } mod_budget_mode;
@@ -120,16 +130,40 @@ mod_status mod_stats_destroy(mod_stats* stats);
 /* Dense warm-up step `step` (Algorithm 1, warm-up phase): fit the MOD
  * coefficients (Eq. 4) on the pooled block-mass statistic of q, k
  * ([B,H,L,d] bf16 device pointers) and record (step, X) as the newest of the
- * two anchors kept.  Steps must strictly increase across collect and
- * predict calls (else MOD_ERR_BAD_STATE). */
+ * two anchors kept.  Steps must strictly increase across collect, update and
+ * predict calls (else MOD_ERR_BAD_STATE).  Statistic 0 only (else
+ * MOD_ERR_BAD_STATE). */
 mod_status mod_collect_stats(mod_stats* stats, const void* q, const void* k, int step,
                              void* stream);
 
+/* Statistic 1 (Section 4.1, Eq. 2 and Eq. 5; Algorithm 1): after the
+ * attention of step `step` -- a dense warm-up step with full lists, or a
+ * re-anchor step with that step's predicted lists -- record the anchor of
+ * that step.  For every listed block (i, j) the informativeness
+ *   I(i, j) = 1 - S(i, j) = fraction of the probabilities
+ *             exp(scale * Q_p.K_q - lse_p), p in i, q in j, that reach eta
+ * (S of Eq. 2 over the block's valid entries; decided in fp32 as
+ * scale * s >= lse_p + log(eta), s the fp32 product of the bf16 inputs)
+ * replaces the stored value; unlisted blocks keep their previous value
+ * (Eq. 5 at block level).  The MOD model is then fitted to the whole stored
+ * map and (step, X) becomes the newest anchor.  The first update should
+ * list every block (the stored map starts at zero).
+ * q, k: [B,H,L,d] bf16 device (the step's inputs, scaled as in the
+ * attention call: scale = 1/sqrt(d)); lse: [B,H,L] fp32 device, the lse the
+ * attention forward returned for these lists; kv_idx, kv_cnt: the lists of
+ * that call (layout of mod_predict_block_mask).  Entries outside [0, n) are
+ * skipped.  `step` must follow the previous call's step, or equal it when
+ * that call was the predict of this step (else MOD_ERR_BAD_STATE).
+ * Statistic 1 only (else MOD_ERR_BAD_STATE). */
+mod_status mod_update_stats(mod_stats* stats, const void* q, const void* k, const float* lse,
+                            const int32_t* kv_idx, const int32_t* kv_cnt, int step, void* stream);
+
 /* Sparse step `step` (Algorithm 1, main phase; Sections 5.2-5.3).
  * On the first call the block-diagonal gate of every head is fixed from the
- * anchors held (gate on iff min over anchors of mean_f e_f > tau_e).  If
- * `step` is a re-anchor step, q and k are pooled and fitted first (else they
- * are not read and may be NULL).  Then c and d are extrapolated to `step`
+ * anchors held (gate on iff min over anchors of mean_f e_f > tau_e).  With
+ * statistic 0, if `step` is a re-anchor step, q and k are pooled and fitted
+ * first (else they are not read and may be NULL); with statistic 1 anchors
+ * come from mod_update_stats only and q, k are never read.  Then c and d are extrapolated to `step`
  * from the two newest anchors (zero slope with one anchor) and every query
  * block i of every head selects key blocks by the score
  *   sigma(i, j) = n * (c~[j - i] + d~[j])
@@ -140,7 +174,7 @@ mod_status mod_collect_stats(mod_stats* stats, const void* q, const void* k, int
  *          holds kv_cnt[(b*H+h)*n+i] ascending block indices; the rest of
  *          the row is not written.
  *   kv_cnt [B, H, n] int32, in [1, n].
- * Requires at least one collected step (else MOD_ERR_BAD_STATE). */
+ * Requires at least one recorded anchor (else MOD_ERR_BAD_STATE). */
 mod_status mod_predict_block_mask(mod_stats* stats, const void* q, const void* k, int step,
                                   const mod_budget* budget, int32_t* kv_idx, int32_t* kv_cnt,
                                   void* stream);
@@ -175,7 +209,8 @@ mod_status mod_stats_get_anchor(const mod_stats* stats, int slot, double* host_c
 /* Block means of the last fitted q, k: [B, H, n, d] fp64 each. */
 mod_status mod_stats_get_pooled(const mod_stats* stats, double* host_qbar, double* host_kbar);
 
-/* Pooled block-mass statistic G of the last fit: [B, H, n, n] fp64. */
+/* The fitted statistic of the last fit: [B, H, n, n] fp64 (statistic 0: the
+ * pooled block mass G; statistic 1: the stored informativeness map I). */
 mod_status mod_stats_get_block_mass(const mod_stats* stats, double* host_G);
 
 /* Last prediction (c~, d~): [B, H, 3n-1] fp64. */

@@ -506,6 +506,7 @@ class Predictor:
         self.scale = 1.0 / math.sqrt(d) if not scale else scale
         self.anchors = []          # list of (t, X [B, H, p])
         self.last_step = None
+        self._last_predict = False
         self.gates = None          # bool [B, H]
         self._N = normal_matrix(self.n, self.regions)
         self.statistic, self.eta = statistic, eta
@@ -530,10 +531,14 @@ class Predictor:
                 X[b, h] = solve_min_norm(self._N, rhs(G[b, h], self.regions), self.n, self.F)
         return X
 
-    def _advance(self, t):
-        if self.last_step is not None and t <= self.last_step:
+    def _advance(self, t, after_predict_ok=False):
+        """Steps increase across calls; an update may also follow the
+        predict of the same step (it uses that step's attention)."""
+        if self.last_step is not None and (t < self.last_step or (
+                t == self.last_step and not (after_predict_ok and self._last_predict))):
             raise ValueError("steps must increase")
         self.last_step = t
+        self._last_predict = False
 
     def collect(self, q, k, t):
         if self.statistic != "pooled":
@@ -553,7 +558,7 @@ class Predictor:
         """Anchor at step t from the statistic of the blocks the step kept
         (current [B, H, n, n], NaN where not kept): Eq. 5 reconstruction,
         then the least-squares fit."""
-        self._advance(t)
+        self._advance(t, after_predict_ok=True)
         self.stat = np.stack([np.stack([reconstruct_statistic(
             None if self.stat is None else self.stat[b, h], current[b, h])
             for h in range(self.H)]) for b in range(self.B)])
@@ -590,6 +595,7 @@ class Predictor:
         if not self.anchors:
             raise ValueError("predict before any collected step")
         self._advance(t)
+        self._last_predict = True
         if self.gates is None:
             self.gates = np.array([[gate([split_coeffs(X[b, h], self.n)[2]
                                           for _, X in self.anchors], self.tau_e)
@@ -619,7 +625,7 @@ class Predictor:
 
 
 def attention_statistic(q: np.ndarray, k: np.ndarray, kept_lists, bs: int, scale: float,
-                        eta: float, lse: np.ndarray | None = None, tol: float = 0.0):
+                        eta: float, lse: np.ndarray | None = None, tol: float = 0.0, rows=None):
     """Eq. 2 on the attention map a step computed: for every kept block
     (i, j), the fraction of its probabilities A(p, q) = exp(scale q_p.k_q -
     LSE_p) that reach eta, where LSE_p normalises over the kept blocks of
@@ -632,14 +638,15 @@ def attention_statistic(q: np.ndarray, k: np.ndarray, kept_lists, bs: int, scale
     against (default: the exact masked LSE).  Returns (I, amb): I [n, n]
     with NaN for blocks not kept; amb [n, n] the number of entries whose
     log-probability lies within tol of log(eta) (where two implementations
-    may round the decision differently).
+    may round the decision differently).  rows: optional subset of query
+    blocks (the other rows stay NaN / 0).
     """
     L = q.shape[0]
     n = num_blocks(L, bs)
     I = np.full((n, n), np.nan)
     amb = np.zeros((n, n), dtype=np.int64)
     log_eta = math.log(eta)
-    for i in range(n):
+    for i in (range(n) if rows is None else rows):
         blocks = list(kept_lists[i])
         if not blocks:
             continue

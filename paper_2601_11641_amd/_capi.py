@@ -41,7 +41,7 @@ class mod_shape(ctypes.Structure):
 
 class mod_params(ctypes.Structure):
     _fields_ = [("warmup_m", c_int), ("delta_t", c_int), ("tau_e", c_float),
-                ("anchor_rule", c_int)]
+                ("anchor_rule", c_int), ("statistic", c_int), ("eta", c_float)]
 
 
 class mod_budget(ctypes.Structure):
@@ -58,7 +58,7 @@ except ImportError:  # pragma: no cover - torch is optional for the ABI itself
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
-                      "(or python -m paper_2601_11641_amd.build_lib)")
+                      "(or python paper_2601_11641_amd/build_lib.py)")
 _lib = ctypes.CDLL(LIB_PATH)
 
 _SIGS = {
@@ -67,6 +67,8 @@ _SIGS = {
     "mod_stats_create": (c_int, [POINTER(mod_shape), POINTER(mod_params), POINTER(c_void_p)]),
     "mod_stats_destroy": (c_int, [c_void_p]),
     "mod_collect_stats": (c_int, [c_void_p, c_void_p, c_void_p, c_int, c_void_p]),
+    "mod_update_stats": (c_int, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_int,
+                                 c_void_p]),
     "mod_predict_block_mask": (c_int, [c_void_p, c_void_p, c_void_p, c_int, POINTER(mod_budget),
                                        c_void_p, c_void_p, c_void_p]),
     "mod_attn_workspace_bytes": (c_size_t, [POINTER(mod_shape)]),
@@ -126,8 +128,9 @@ def make_shape(B, H, L, d, block, frame_tokens=0) -> mod_shape:
     return mod_shape(B, H, L, d, block, frame_tokens)
 
 
-def make_params(warmup_m=1, delta_t=0, tau_e=0.0, anchor_rule=0) -> mod_params:
-    return mod_params(warmup_m, delta_t, tau_e, anchor_rule)
+def make_params(warmup_m=1, delta_t=0, tau_e=0.0, anchor_rule=0, statistic=0, eta=1e-4) -> mod_params:
+    s = {"pooled": 0, "attention": 1}.get(statistic, statistic)
+    return mod_params(warmup_m, delta_t, tau_e, anchor_rule, int(s), eta)
 
 
 def make_budget(mode="topk", density=1.0, mass=1.0, patterns=1) -> mod_budget:
@@ -164,6 +167,13 @@ def mod_collect_stats(stats, q, k, step: int, stream=None) -> None:
     _check(_lib.mod_collect_stats(stats, _ptr(q, "q", "torch.bfloat16"),
                                   _ptr(k, "k", "torch.bfloat16"), step, _stream(stream)),
            "mod_collect_stats")
+
+
+def mod_update_stats(stats, q, k, lse, kv_idx, kv_cnt, step: int, stream=None) -> None:
+    _check(_lib.mod_update_stats(stats, _ptr(q, "q", "torch.bfloat16"), _ptr(k, "k", "torch.bfloat16"),
+                                 _ptr(lse, "lse", "torch.float32"), _ptr(kv_idx, "kv_idx", "torch.int32"),
+                                 _ptr(kv_cnt, "kv_cnt", "torch.int32"), step, _stream(stream)),
+           "mod_update_stats")
 
 
 def mod_predict_block_mask(stats, q, k, step: int, budget: mod_budget, kv_idx, kv_cnt,

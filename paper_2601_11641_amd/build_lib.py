@@ -1,6 +1,7 @@
 """Build libmoddit.so (gfx950) in-tree with hipcc.
 
-Usage: python -m paper_2601_11641_amd.build_lib  (or build() from Python).
+Usage: python paper_2601_11641_amd/build_lib.py (or __graft_entry__.build()); run
+by path, since importing the package needs the library.
 Every call recompiles; objects go to paper_2601_11641_amd/_build/.
 """
 from __future__ import annotations

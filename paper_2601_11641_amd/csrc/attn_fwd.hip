@@ -194,8 +194,9 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     // ---- union of the kv lists of blocks 2p and 2p+1, ascending j ----
     // (entries outside [0, n) are ignored; a repeated entry counts once)
     const int i0 = 2 * pr, i1 = 2 * pr + 1;
-    const int cnt0 = kv_cnt[bh * n + i0];
-    const int cnt1 = i1 < n ? kv_cnt[bh * n + i1] : 0;
+    // counts are clamped to [0, n]: a row never reads past its n entries
+    const int cnt0 = min(max(kv_cnt[bh * n + i0], 0), n);
+    const int cnt1 = i1 < n ? min(max(kv_cnt[bh * n + i1], 0), n) : 0;
     const int32_t* list0 = kv_idx + (size_t)(bh * n + i0) * n;
     const int32_t* list1 = list0 + n;
     for (int j = tid; j < n; j += NT) umask[j] = 0;
@@ -523,6 +524,110 @@ hipError_t launch(const uint16_t* q, const uint16_t* k, const uint16_t* v, const
     return hipGetLastError();
 }
 
+
+// ---------------------------------------------------------------------------
+// Eq. 2 statistic of the attention map a step computed: for every listed
+// block (i, j), the fraction of the probabilities exp(scale q_p.k_q - LSE_p)
+// that reach eta, LSE_p being the row LSE the attention forward returned
+// over the same lists (the masked map; all blocks at a dense step).  The
+// decision is taken in fp32: scale * s >= LSE_p + log(eta), s the fp32 MFMA
+// product.  One work-group per (head, query block), BS/32 waves of 32 query
+// rows; the K tiles of the row's list are copied into LDS one tile ahead.
+// The result is written into stat[bh][i][j] (fp64); blocks not listed keep
+// their previous value (the reconstruction of Eq. 5).
+// ---------------------------------------------------------------------------
+template <int D, int BS>
+__global__ __launch_bounds__(BS * 2, 1) void stat_count_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+    const int32_t* __restrict__ kv_idx, const int32_t* __restrict__ kv_cnt,
+    const float* __restrict__ lse, float scale, float log_eta, double* __restrict__ stat, int L, int n) {
+    constexpr int QW = BS / 32;        // waves, 32 query rows each
+    constexpr int RT = BS / 32;        // 32-row kv sub-tiles per tile
+    constexpr int KK = D / 16;
+    constexpr int TILE = BS * D * 2;
+    constexpr int ROWB = 2 * D;
+    using Copy = TileCopy<D, BS, QW>;
+    __shared__ __align__(1024) char kb0[TILE];
+    __shared__ __align__(1024) char kb1[TILE];
+    __shared__ int part[2][QW];
+
+    const int item = blockIdx.x;       // bh * n + i
+    const int bh = item / n, i = item % n;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int h = lane >> 5, l32 = lane & 31;
+    const size_t base = (size_t)bh * L * D;
+    const int qrow = i * BS + 32 * w + l32;
+    const int rows_i = min(BS, L - i * BS);
+
+    bf16x8 qreg[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+        uint4 val = make_uint4(0, 0, 0, 0);
+        if (qrow < L)
+            val = *reinterpret_cast<const uint4*>(q + base + (size_t)qrow * D + 16 * kk + 8 * h);
+        qreg[kk] = __builtin_bit_cast(bf16x8, val);
+    }
+    // a row past the end of the sequence never counts
+    const float thr = qrow < L ? lse[(size_t)bh * L + qrow] + log_eta : INFINITY;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) asm volatile("" : "+v"(qreg[kk]));
+
+    const int cnt = min(max(kv_cnt[item], 0), n);   // never past the row's n entries
+    const int32_t* list = kv_idx + (size_t)item * n;
+    const Copy copy(lane);
+    const uint16_t* kg = k + base;
+    const int ka = l32 * ROWB + ((h ^ swz<D>(l32)) << 4);
+    // entries outside [0, n) are skipped (their copy reads block 0)
+    auto block_of = [&](int t) { const int j = list[t]; return (unsigned)j < (unsigned)n ? j : -1; };
+    if (cnt > 0) copy.issue_all(kg, max(block_of(0), 0), L, kb0, w, lane);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    for (int t = 0; t < cnt; ++t) {
+        const char* cur = (t & 1) ? kb1 : kb0;
+        char* nxt = (t & 1) ? kb0 : kb1;
+        if (t + 1 < cnt) copy.issue_all(kg, max(block_of(t + 1), 0), L, nxt, w, lane);
+        const int j = block_of(t);
+        const int kvalid = j < 0 ? 0 : min(BS, L - j * BS);
+        int c = 0;
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            f32x16 sv = f32x16{};
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                const bf16x8 a = __builtin_bit_cast(
+                    bf16x8, *reinterpret_cast<const uint4*>(cur + ((ka ^ (32 * kk)) + 32 * rt * ROWB)));
+                sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sv, 0, 0, 0);
+            }
+#pragma unroll
+            for (int ii = 0; ii < 16; ++ii) {
+                const int kv = 32 * rt + 8 * (ii >> 2) + 4 * h + (ii & 3);
+                c += (kv < kvalid && sv[ii] * scale >= thr) ? 1 : 0;
+            }
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
+        if (lane == 0) part[t & 1][w] = c;
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        if (tid == 0 && j >= 0) {
+            int total = 0;
+#pragma unroll
+            for (int ww = 0; ww < QW; ++ww) total += part[t & 1][ww];
+            stat[(size_t)item * n + j] = (double)total / ((double)rows_i * (double)kvalid);
+        }
+    }
+}
+
+template <int D, int BS>
+hipError_t launch_count(const uint16_t* q, const uint16_t* k, const int32_t* kv_idx, const int32_t* kv_cnt,
+                        const float* lse, float scale, float log_eta, double* stat, int BH, int L, int n,
+                        hipStream_t s) {
+    hipLaunchKernelGGL((stat_count_kernel<D, BS>), dim3((unsigned)BH * n), dim3(BS * 2), 0, s, q, k, kv_idx,
+                       kv_cnt, lse, scale, log_eta, stat, L, n);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v,
@@ -533,6 +638,15 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
     if (d == 128 && bs == 64) return launch<128, 64>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, s);
     if (d == 64 && bs == 128) return launch<64, 128>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, s);
     return launch<64, 64>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, s);
+}
+
+hipError_t launch_stat_count(const uint16_t* q, const uint16_t* k, const int32_t* kv_idx,
+                             const int32_t* kv_cnt, const float* lse, float scale, float log_eta,
+                             double* stat, int BH, int L, int d, int bs, int n, hipStream_t s) {
+    if (d == 128 && bs == 128) return launch_count<128, 128>(q, k, kv_idx, kv_cnt, lse, scale, log_eta, stat, BH, L, n, s);
+    if (d == 128 && bs == 64) return launch_count<128, 64>(q, k, kv_idx, kv_cnt, lse, scale, log_eta, stat, BH, L, n, s);
+    if (d == 64 && bs == 128) return launch_count<64, 128>(q, k, kv_idx, kv_cnt, lse, scale, log_eta, stat, BH, L, n, s);
+    return launch_count<64, 64>(q, k, kv_idx, kv_cnt, lse, scale, log_eta, stat, BH, L, n, s);
 }
 
 }  // namespace moddit

@@ -201,6 +201,7 @@ struct mod_stats {
     int anchor_step[2] = {0, 0};
     bool has_step = false;
     int last_step = 0;
+    bool last_predicted = false;   // the last call was the predict of last_step
     bool gate_frozen = false;
     bool fitted = false;
     bool predicted = false;
@@ -224,17 +225,10 @@ bool is_anchor_step(const mod_stats* s, int t) {
     return t % dt == 0;
 }
 
-// pool -> block mass -> rhs -> solve into the next anchor slot
-mod_status fit_into_next_slot(mod_stats* s, const void* q, const void* k, int step,
-                              hipStream_t st) {
-    const mod_shape& sh = s->shape;
+// rhs -> solve of the statistic in G into the next anchor slot
+mod_status fit_stat_into_next_slot(mod_stats* s, int step, hipStream_t st) {
     const int slot = 1 - s->newest;
-    hipError_t e = moddit::launch_pool(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-                                       s->qbar, s->kbar, s->BH, sh.L, sh.d, sh.block, s->n, st);
-    if (e != hipSuccess) return hip_fail(e, "pool launch");
-    e = moddit::launch_block_mass(s->qbar, s->kbar, s->G, s->BH, sh.L, sh.d, sh.block, s->n, s->scale, st);
-    if (e != hipSuccess) return hip_fail(e, "block-mass launch");
-    e = moddit::launch_rhs(s->G, s->reg, s->r, s->BH, s->n, s->F, st);
+    hipError_t e = moddit::launch_rhs(s->G, s->reg, s->r, s->BH, s->n, s->F, st);
     if (e != hipSuccess) return hip_fail(e, "rhs launch");
     e = moddit::launch_solve(s->r, s->reg, s->Sinv, s->bU, s->u, s->X[slot], s->BH, s->n, s->F, st);
     if (e != hipSuccess) return hip_fail(e, "solve launch");
@@ -245,8 +239,27 @@ mod_status fit_into_next_slot(mod_stats* s, const void* q, const void* k, int st
     return MOD_OK;
 }
 
+// pool -> block mass -> rhs -> solve into the next anchor slot (statistic 0)
+mod_status fit_into_next_slot(mod_stats* s, const void* q, const void* k, int step,
+                              hipStream_t st) {
+    const mod_shape& sh = s->shape;
+    hipError_t e = moddit::launch_pool(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                                       s->qbar, s->kbar, s->BH, sh.L, sh.d, sh.block, s->n, st);
+    if (e != hipSuccess) return hip_fail(e, "pool launch");
+    e = moddit::launch_block_mass(s->qbar, s->kbar, s->G, s->BH, sh.L, sh.d, sh.block, s->n, s->scale, st);
+    if (e != hipSuccess) return hip_fail(e, "block-mass launch");
+    return fit_stat_into_next_slot(s, step, st);
+}
+
 mod_status check_step(const mod_stats* s, int step) {
     if (s->has_step && step <= s->last_step)
+        return fail(MOD_ERR_BAD_STATE, "step %d does not follow step %d", step, s->last_step);
+    return MOD_OK;
+}
+
+// an update may also follow the predict of the same step (its attention)
+mod_status check_update_step(const mod_stats* s, int step) {
+    if (s->has_step && (step < s->last_step || (step == s->last_step && !s->last_predicted)))
         return fail(MOD_ERR_BAD_STATE, "step %d does not follow step %d", step, s->last_step);
     return MOD_OK;
 }
@@ -276,6 +289,10 @@ mod_status mod_stats_create(const mod_shape* shape, const mod_params* params, mo
     if (params->anchor_rule != 0 && params->anchor_rule != 1)
         return fail(MOD_ERR_INVALID_ARG, "anchor_rule must be 0 or 1");
     if (!std::isfinite(params->tau_e)) return fail(MOD_ERR_INVALID_ARG, "tau_e must be finite");
+    if (params->statistic != 0 && params->statistic != 1)
+        return fail(MOD_ERR_INVALID_ARG, "statistic must be 0 or 1");
+    if (params->statistic == 1 && !(params->eta > 0.0f && std::isfinite(params->eta)))
+        return fail(MOD_ERR_INVALID_ARG, "eta must be positive and finite");
 
     mod_stats* s = new (std::nothrow) mod_stats();
     if (!s) return fail(MOD_ERR_NOMEM, "host allocation failed");
@@ -338,6 +355,7 @@ mod_status mod_stats_create(const mod_shape* shape, const mod_params* params, mo
     if (e == hipSuccess) e = hipMemcpy(s->row_lo, row_lo.data(), n * sizeof(int), hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(s->row_hi, row_hi.data(), n * sizeof(int), hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemset(s->gate, 0, BH * sizeof(int32_t));
+    if (e == hipSuccess) e = hipMemset(s->G, 0, BH * n * n * sizeof(double));
     if (e == hipSuccess) e = hipDeviceSynchronize();
     if (e != hipSuccess) {
         free_stats(s);
@@ -358,12 +376,39 @@ mod_status mod_stats_destroy(mod_stats* stats) {
 mod_status mod_collect_stats(mod_stats* s, const void* q, const void* k, int step, void* stream) {
     if (!s) return fail(MOD_ERR_INVALID_ARG, "stats is NULL");
     if (!q || !k) return fail(MOD_ERR_INVALID_ARG, "q and k must not be NULL");
+    if (s->params.statistic != 0)
+        return fail(MOD_ERR_BAD_STATE, "statistic 1 records anchors with mod_update_stats");
     mod_status st = check_step(s, step);
     if (st != MOD_OK) return st;
     st = fit_into_next_slot(s, q, k, step, static_cast<hipStream_t>(stream));
     if (st != MOD_OK) return st;
     s->has_step = true;
     s->last_step = step;
+    s->last_predicted = false;
+    return MOD_OK;
+}
+
+mod_status mod_update_stats(mod_stats* s, const void* q, const void* k, const float* lse,
+                            const int32_t* kv_idx, const int32_t* kv_cnt, int step, void* stream) {
+    if (!s) return fail(MOD_ERR_INVALID_ARG, "stats is NULL");
+    if (!q || !k || !lse || !kv_idx || !kv_cnt)
+        return fail(MOD_ERR_INVALID_ARG, "q, k, lse, kv_idx and kv_cnt must not be NULL");
+    if (s->params.statistic != 1)
+        return fail(MOD_ERR_BAD_STATE, "mod_update_stats needs statistic 1");
+    mod_status st = check_update_step(s, step);
+    if (st != MOD_OK) return st;
+    const mod_shape& sh = s->shape;
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    hipError_t e = moddit::launch_stat_count(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                                             kv_idx, kv_cnt, lse, (float)s->scale,
+                                             (float)std::log((double)s->params.eta), s->G, s->BH, sh.L, sh.d,
+                                             sh.block, s->n, hs);
+    if (e != hipSuccess) return hip_fail(e, "statistic launch");
+    st = fit_stat_into_next_slot(s, step, hs);
+    if (st != MOD_OK) return st;
+    s->has_step = true;
+    s->last_step = step;
+    s->last_predicted = false;
     return MOD_OK;
 }
 
@@ -394,7 +439,7 @@ mod_status mod_predict_block_mask(mod_stats* s, const void* q, const void* k, in
     if (s->n_anchors == 0) return fail(MOD_ERR_BAD_STATE, "predict before any collected step");
     mod_status st = check_step(s, step);
     if (st != MOD_OK) return st;
-    const bool anchor = is_anchor_step(s, step);
+    const bool anchor = s->params.statistic == 0 && is_anchor_step(s, step);
     if (anchor && (!q || !k))
         return fail(MOD_ERR_INVALID_ARG, "step %d re-anchors: q and k must not be NULL", step);
     hipStream_t hs = static_cast<hipStream_t>(stream);
@@ -429,6 +474,7 @@ mod_status mod_predict_block_mask(mod_stats* s, const void* q, const void* k, in
     if (e != hipSuccess) return hip_fail(e, "select launch");
     s->has_step = true;
     s->last_step = step;
+    s->last_predicted = true;
     s->predicted = true;
     return MOD_OK;
 }

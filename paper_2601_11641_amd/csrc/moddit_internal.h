@@ -55,4 +55,12 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
                            uint16_t* o, float* lse, int BH, int L, int d, int bs, int n,
                            hipStream_t s);
 
+// Eq. 2 statistic of a computed attention map: stat[bh][i][j] = fraction of
+// the probabilities of listed block (i, j) that reach exp(log_eta), with the
+// row LSE of the attention forward over the same lists; unlisted blocks keep
+// their value.
+hipError_t launch_stat_count(const uint16_t* q, const uint16_t* k, const int32_t* kv_idx,
+                             const int32_t* kv_cnt, const float* lse, float scale, float log_eta,
+                             double* stat, int BH, int L, int d, int bs, int n, hipStream_t s);
+
 }  // namespace moddit

@@ -15,8 +15,8 @@ LIB = os.path.join(ROOT, "paper_2601_11641_amd", "libmoddit.so")
 @pytest.fixture(scope="module")
 def M():
     if not os.path.exists(LIB):
-        from paper_2601_11641_amd import build_lib
-        build_lib.build()
+        import __graft_entry__
+        __graft_entry__.build()
     import paper_2601_11641_amd as m
     return m
 
@@ -105,7 +105,8 @@ def test_struct_layouts_match_the_header(M, tmp_path):
         '  printf("%zu %zu %zu %zu %zu\\n", sizeof(mod_budget), offsetof(mod_budget, mode),\n'
         '         offsetof(mod_budget, density), offsetof(mod_budget, mass), offsetof(mod_budget, patterns));\n'
         '  printf("%zu %zu\\n", sizeof(mod_shape), offsetof(mod_shape, frame_tokens));\n'
-        '  printf("%zu %zu\\n", sizeof(mod_params), offsetof(mod_params, anchor_rule));\n'
+        '  printf("%zu %zu %zu\\n", sizeof(mod_params), offsetof(mod_params, anchor_rule),\n'
+        '         offsetof(mod_params, eta));\n'
         '  return 0;\n}\n')
     exe = tmp_path / "layout"
     subprocess.run([cc, "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
@@ -114,5 +115,5 @@ def test_struct_layouts_match_the_header(M, tmp_path):
     want = [ctypes.sizeof(M.mod_budget), M.mod_budget.mode.offset, M.mod_budget.density.offset,
             M.mod_budget.mass.offset, M.mod_budget.patterns.offset,
             ctypes.sizeof(M.mod_shape), M.mod_shape.frame_tokens.offset,
-            ctypes.sizeof(M.mod_params), M.mod_params.anchor_rule.offset]
+            ctypes.sizeof(M.mod_params), M.mod_params.anchor_rule.offset, M.mod_params.eta.offset]
     assert got == want

@@ -1,0 +1,207 @@
+"""GPU parity of the attention sparsity statistic (Eq. 2, statistic 1) and
+its block-level reconstruction (Eq. 5) through the C ABI.
+
+The count of probabilities reaching eta is an integer decided in floating
+point; the GPU decides in fp32 (scale * s >= lse + log eta) and the oracle in
+fp64 against the GPU's own lse, so per block the counts may differ only by
+entries whose log-probability lies within TOL of log(eta).  The fit, the
+extrapolation and the selection are then checked against the oracle fed
+with the GPU's statistic (decoupled from those boundary entries)."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from parity import bf16_tensor, compare_lists, gpu_lists
+
+import paper_2601_11641_amd as M
+
+torch = pytest.importorskip("torch")
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+TOL = 2e-4     # log-space window around log(eta) where fp32 and fp64 may disagree
+ETA = 1e-4
+
+
+def _cfg(base, **kw):
+    c = W.CONFIGS[base]
+    d = dict(name=c.name, B=c.B, H=c.H, d=c.d, frames=c.frames, hs=c.hs, ws=c.ws,
+             block=c.block, seed=c.seed)
+    d.update(kw)
+    return W.LayerConfig(**d)
+
+
+CONFIGS = {
+    "tiny": W.CONFIGS["tiny"],
+    "small3": _cfg("small", H=3),
+    # ragged: short tail block, frames straddling blocks
+    "ragged": _cfg("small", name="ragged", B=2, H=2, frames=5, hs=9, ws=25, seed=5),
+}
+
+
+def _device(cfg):
+    host = W.generate(cfg)
+    return host, tuple(bf16_tensor(x) for x in host)
+
+
+def _lists_tensors(cfg, rows):
+    n = cfg.n
+    idx = torch.zeros((cfg.B, cfg.H, n, n), dtype=torch.int32)
+    cnt = torch.zeros((cfg.B, cfg.H, n), dtype=torch.int32)
+    for b in range(cfg.B):
+        for h in range(cfg.H):
+            for i, js in enumerate(rows[b][h]):
+                cnt[b, h, i] = len(js)
+                idx[b, h, i, :len(js)] = torch.tensor(js, dtype=torch.int32)
+    return idx.cuda(), cnt.cuda()
+
+
+def _attention(cfg, dev, idx, cnt):
+    qd, kd, vd = dev
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    o = torch.empty_like(qd)
+    lse = torch.empty((cfg.B, cfg.H, cfg.L), dtype=torch.float32, device="cuda")
+    M.mod_block_sparse_attn_fwd(shape, qd, kd, vd, idx, cnt, 0.0, o, lse)
+    return lse
+
+
+def _check_counts(cfg, host, lse, rows, stat_before, stat_after):
+    """Listed blocks: counts within the boundary entries; others unchanged."""
+    n = cfg.n
+    sizes = O.block_sizes(cfg.L, cfg.block)
+    lg = lse.cpu().numpy().astype(np.float64)
+    for b in range(cfg.B):
+        for h in range(cfg.H):
+            qf, kf = W.bf16_bits_to_f64(host[0][b, h]), W.bf16_bits_to_f64(host[1][b, h])
+            I, amb = O.attention_statistic(qf, kf, rows[b][h], cfg.block, 1.0 / math.sqrt(cfg.d), ETA,
+                                           lse=lg[b, h], tol=TOL)
+            listed = ~np.isnan(I)
+            got = stat_after[b, h]
+            cnt_diff = np.abs(got - np.nan_to_num(I)) * np.outer(sizes, sizes)
+            assert (cnt_diff[listed] <= amb[listed] + 1e-6).all(), \
+                (b, h, float(cnt_diff[listed].max()), int(amb[listed].max()))
+            if stat_before is not None:
+                assert (got[~listed] == stat_before[b, h][~listed]).all()
+
+
+@pytest.mark.parametrize("name", sorted(CONFIGS))
+def test_statistic_schedule(name):
+    """Dense warm-up updates at steps 1 and 2, predictions at 3..5, a sparse
+    re-anchor update at step 4 (Eq. 5: only the listed blocks change), and
+    the masks of every predicted step against the oracle fed with the
+    GPU's statistic."""
+    cfg = CONFIGS[name]
+    host, dev = _device(cfg)
+    qd, kd, _ = dev
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    params = dict(warmup_m=2, delta_t=2, tau_e=0.0)
+    st = M.Stats(shape, M.make_params(statistic="attention", eta=ETA, **params))
+    n, B, H = st.n, cfg.B, cfg.H
+    P = O.Predictor(B, H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens, statistic="attention", eta=ETA,
+                    **params)
+    full = [[[list(range(n))] * n for _ in range(H)] for _ in range(B)]
+    fidx, fcnt = _lists_tensors(cfg, full)
+    before = None
+    for t in (1, 2):                                   # dense warm-up steps
+        lse = _attention(cfg, dev, fidx, fcnt)
+        M.mod_update_stats(st.handle, qd, kd, lse, fidx, fcnt, t)
+        torch.cuda.synchronize()
+        after = M.mod_stats_get_block_mass(st.handle, B, H, n)
+        _check_counts(cfg, host, lse, full, before, after)
+        before = after
+        cur = np.where(np.ones((B, H, n, n), bool), after, np.nan)
+        P.update_from_statistic(cur, t)
+    idx = torch.empty((B, H, n, n), dtype=torch.int32, device="cuda")
+    cnt = torch.empty((B, H, n), dtype=torch.int32, device="cuda")
+    budget = ("topk", 0.4)
+    for t in (3, 4, 5):
+        M.mod_predict_block_mask(st.handle, None, None, t, M.make_budget("topk", density=0.4), idx, cnt)
+        torch.cuda.synchronize()
+        X, t2 = M.mod_stats_get_anchor(st.handle, 0, B, H, st.p)
+        assert t2 == P.anchors[-1][0]
+        assert np.abs(X - P.anchors[-1][1]).max() <= 1e-9 * max(1.0, np.abs(P.anchors[-1][1]).max())
+        sel = P.predict(None, None, t, O.Budget("topk", density=0.4))
+        rows = gpu_lists(idx, cnt)
+        po = P.prediction(t)
+        k = O.topk_count(0.4, n)
+        total = excused = 0
+        for b in range(B):
+            for h in range(H):
+                sig = O.scores(*po[b][h], n)
+                forced = O.forced_mask(n, P.regions, bool(P.gates[b, h]))
+                nr, _, nx, bad = compare_lists(rows[b][h], sel[b][h], sig, forced, budget[0], k)
+                assert not bad, (t, b, h, bad[:10])
+                total, excused = total + nr, excused + nx
+        assert excused <= max(2, 0.02 * total)
+        if t == 4:                                     # re-anchor from the sparse step's attention
+            lse = _attention(cfg, dev, idx, cnt)
+            M.mod_update_stats(st.handle, qd, kd, lse, idx, cnt, t)
+            torch.cuda.synchronize()
+            after = M.mod_stats_get_block_mass(st.handle, B, H, n)
+            _check_counts(cfg, host, lse, rows, before, after)
+            listed = np.zeros((B, H, n, n), bool)
+            for b in range(B):
+                for h in range(H):
+                    for i, js in enumerate(rows[b][h]):
+                        listed[b, h, i, js] = True
+            P.update_from_statistic(np.where(listed, after, np.nan), t)
+            before = after
+    st.close()
+
+
+def test_statistic_state_errors():
+    cfg = W.CONFIGS["tiny"]
+    _, dev = _device(cfg)
+    qd, kd, _ = dev
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    n = M.mod_num_blocks(shape)
+    for bad in (0.0, -1.0, float("inf")):
+        with pytest.raises(M.ModError) as e:
+            M.Stats(shape, M.make_params(statistic="attention", eta=bad))
+        assert e.value.status == M.MOD_ERR_INVALID_ARG
+    st = M.Stats(shape, M.make_params(warmup_m=1, statistic="attention"))
+    with pytest.raises(M.ModError) as e:
+        M.mod_collect_stats(st.handle, qd, kd, 1)
+    assert e.value.status == M.MOD_ERR_BAD_STATE
+    st.close()
+    st = M.Stats(shape, M.make_params(warmup_m=1))
+    idx = torch.zeros((cfg.B, cfg.H, n, n), dtype=torch.int32, device="cuda")
+    cnt = torch.zeros((cfg.B, cfg.H, n), dtype=torch.int32, device="cuda")
+    lse = torch.zeros((cfg.B, cfg.H, cfg.L), dtype=torch.float32, device="cuda")
+    with pytest.raises(M.ModError) as e:
+        M.mod_update_stats(st.handle, qd, kd, lse, idx, cnt, 1)
+    assert e.value.status == M.MOD_ERR_BAD_STATE
+    st.close()
+
+
+def test_statistic_720p_dense_sampled_rows():
+    """Dense warm-up statistic on the Hunyuan 720p layer: sampled query
+    blocks of two heads against the oracle."""
+    cfg = W.CONFIGS["hunyuan"]
+    host, dev = _device(cfg)
+    qd, kd, _ = dev
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    st = M.Stats(shape, M.make_params(warmup_m=1, statistic="attention", eta=ETA))
+    n = st.n
+    fidx = torch.arange(n, dtype=torch.int32, device="cuda").repeat(cfg.H * n).reshape(1, cfg.H, n, n)
+    fcnt = torch.full((1, cfg.H, n), n, dtype=torch.int32, device="cuda")
+    lse = _attention(cfg, dev, fidx, fcnt)
+    M.mod_update_stats(st.handle, qd, kd, lse, fidx, fcnt, 1)
+    torch.cuda.synchronize()
+    got = M.mod_stats_get_block_mass(st.handle, 1, cfg.H, n)
+    lg = lse.cpu().numpy().astype(np.float64)
+    sizes = O.block_sizes(cfg.L, cfg.block)
+    rng = np.random.default_rng(3)
+    for h in (0, cfg.H - 1):
+        sub = W.generate_heads(cfg, heads=[h])
+        qf, kf = W.bf16_bits_to_f64(sub[0][0, 0]), W.bf16_bits_to_f64(sub[1][0, 0])
+        rows = sorted(set(rng.choice(n - 1, size=3, replace=False).tolist()) | {n - 1})
+        I, amb = O.attention_statistic(qf, kf, [list(range(n))] * n, cfg.block, 1.0 / math.sqrt(cfg.d),
+                                       ETA, lse=lg[0, h], tol=TOL, rows=rows)
+        for i in rows:
+            diff = np.abs(got[0, h, i] - I[i]) * sizes[i] * sizes
+            assert (diff <= amb[i] + 1e-6).all(), (h, i, float(diff.max()))
+    st.close()
