@@ -310,6 +310,38 @@ def forced_mask(n: int, regions, gate_on: bool) -> np.ndarray:
     return m
 
 
+def text_blocks(L_video: int, L: int, bs: int) -> range:
+    """Blocks holding at least one text token when a text segment of
+    L - L_video tokens follows the video tokens (token-type-aware masking,
+    Section 3); empty without text.  A block holding the last video tokens
+    and the first text tokens counts as a text block."""
+    if L == L_video:
+        return range(0)
+    return range(L_video // bs, num_blocks(L, bs))
+
+
+def add_text(rows_video, L_video: int, L: int, bs: int):
+    """Token-type-aware masking (Section 3): text tokens attend to and are
+    attended by every token.  At block level (reading): the rows of text
+    blocks keep every block; every other row keeps its video selection plus
+    every text block.  rows_video: RowSelection per video query block (the
+    selection over the video blocks, the mixed block already forced).
+    Returns one RowSelection per block of the whole sequence."""
+    n = num_blocks(L, bs)
+    tb = text_blocks(L_video, L, bs)
+    if len(tb) == 0:
+        return list(rows_video)
+    out = []
+    for i in range(n):
+        if i in tb:
+            out.append(RowSelection(np.arange(n), math.inf, math.inf))
+        else:
+            r = rows_video[i]
+            kept = np.union1d(r.kept, np.arange(tb.start, n))
+            out.append(RowSelection(kept, r.key_gap, r.mass_margin))
+    return out
+
+
 def topk_count(density: float, n: int) -> int:
     """k = clamp(ceil(rho * n), 1, n), with rho taken at float32 precision
     and a 1e-6 guard so that an integral rho*n is not pushed up by rounding."""
@@ -496,9 +528,15 @@ class Predictor:
     """
 
     def __init__(self, B, H, L, d, bs, frame_tokens, warmup_m, delta_t, tau_e=0.0,
-                 anchor_rule=0, scale=None, statistic="pooled", eta=1e-4):
+                 anchor_rule=0, scale=None, statistic="pooled", eta=1e-4, text_tokens=0):
+        # the MOD machinery runs over the video tokens; a text segment of
+        # text_tokens tokens after them only changes the output lists
+        self.L_total = L
+        self.n_total = num_blocks(L, bs)
+        L = L - text_tokens
         self.B, self.H, self.L, self.d, self.bs = B, H, L, d, bs
         self.n = num_blocks(L, bs)
+        self.text = text_blocks(L, self.L_total, bs)
         self.regions = frame_regions(L, bs, frame_tokens)
         self.F = len(self.regions)
         self.sizes = block_sizes(L, bs)
@@ -512,6 +550,15 @@ class Predictor:
         self.statistic, self.eta = statistic, eta
         self.stat = None           # "attention": reconstructed map [B, H, n, n]
 
+    def forced(self, gate_on: bool) -> np.ndarray:
+        """Forced video blocks: K_E when the gate is on, plus the block that
+        holds the last video tokens and the first text tokens (a text block
+        on the key side)."""
+        f = forced_mask(self.n, self.regions, gate_on)
+        if len(self.text) and self.text.start < self.n:
+            f[:, self.text.start] = True
+        return f
+
     def is_anchor_step(self, t: int) -> bool:
         if self.dt <= 0:
             return False
@@ -520,6 +567,7 @@ class Predictor:
         return t % self.dt == 0
 
     def pooled_mass(self, q, k):
+        q, k = q[..., :self.L, :], k[..., :self.L, :]
         qb, kb = pool(q, self.bs), pool(k, self.bs)
         return block_mass(qb, kb, self.sizes, self.scale)
 
@@ -575,7 +623,8 @@ class Predictor:
         for b in range(self.B):
             for h in range(self.H):
                 cur[b, h] = attention_statistic(q[b, h], k[b, h], kept[b][h], self.bs, self.scale,
-                                                self.eta, None if lse is None else lse[b, h])[0]
+                                                self.eta, None if lse is None else lse[b, h]
+                                                )[0][:self.n, :self.n]
         self.update_from_statistic(cur, t)
 
     def prediction(self, t):
@@ -609,12 +658,13 @@ class Predictor:
             row = []
             for h in range(self.H):
                 ct, dt_ = pred[b][h]
-                forced = forced_mask(self.n, self.regions, bool(self.gates[b, h]))
+                forced = self.forced(bool(self.gates[b, h]))
                 if budget.mode == "pattern":
-                    row.append(select_patterns(ct, dt_, self.n, budget.patterns, forced))
-                    continue
-                sig = scores(ct, dt_, self.n)
-                row.append(select(sig, forced, budget.mode, budget.density, budget.mass))
+                    sel = select_patterns(ct, dt_, self.n, budget.patterns, forced)
+                else:
+                    sig = scores(ct, dt_, self.n)
+                    sel = select(sig, forced, budget.mode, budget.density, budget.mass)
+                row.append(add_text(sel, self.L, self.L_total, self.bs))
             result.append(row)
         return result
 

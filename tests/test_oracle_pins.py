@@ -399,6 +399,67 @@ def test_pattern_topk_invariants():
             assert (j in r.kept) == (covered or forced[i, j])
 
 
+# ------------------------------------------------- token-type-aware masking
+
+def _text_case(text_tokens, frames, hh, ww, seed=11):
+    rng = np.random.default_rng(seed)
+    Lv = frames * hh * ww
+    L = Lv + text_tokens
+    q, k = rng.standard_normal((1, 2, L, 16)), rng.standard_normal((1, 2, L, 16))
+    return Lv, L, q, k
+
+
+@pytest.mark.parametrize("shape", [(4, 8, 8, 64), (4, 8, 8, 40), (4, 5, 10, 50)])
+@pytest.mark.parametrize("mode", ["topk", "mass", "pattern"])
+def test_text_rows_and_columns_full_and_video_part(shape, mode):
+    """Text blocks' rows keep everything and every row keeps the text blocks.
+    Aligned text: the video part of a row is exactly the video-only
+    predictor's selection.  Text starting inside a block (shape 3): that
+    block is forced into every row, and in TOPK the other video blocks are
+    the frame blocks forced by the gate plus the best-scoring others of the
+    video-only prediction, the shared block taking one of the k places."""
+    frames, hh, ww, text_tokens = shape
+    bs = 32
+    Lv, L, q, k = _text_case(text_tokens, frames, hh, ww)
+    budget = O.Budget(mode, density=0.3, mass=0.6, patterns=9)
+    kw = dict(warmup_m=1, delta_t=0)
+    P = O.Predictor(1, 2, L, 16, bs, hh * ww, text_tokens=text_tokens, **kw)
+    V = O.Predictor(1, 2, Lv, 16, bs, hh * ww, **kw)
+    P.collect(q, k, 1)
+    V.collect(q[..., :Lv, :], k[..., :Lv, :], 1)
+    rows = P.predict(q, k, 2, budget)[0]
+    vrows = V.predict(q[..., :Lv, :], k[..., :Lv, :], 2, budget)[0]
+    n, nv = O.num_blocks(L, bs), O.num_blocks(Lv, bs)
+    tb = list(range(Lv // bs, n))
+    mixed = Lv % bs != 0
+    kk = O.topk_count(0.3, nv)
+    for h in range(2):
+        assert len(rows[h]) == n
+        ct, dt_ = V.prediction(2)[0][h]
+        keys = O.scores(ct, dt_, nv).astype(np.float32)
+        for i in range(n):
+            kept = rows[h][i].kept.tolist()
+            if i in tb:
+                assert kept == list(range(n))
+                continue
+            assert set(tb) <= set(kept)
+            video = [j for j in kept if j not in tb]
+            if not mixed:
+                assert video == vrows[h][i].kept.tolist()
+            elif mode == "topk":
+                forced = set(np.flatnonzero(O.forced_mask(nv, V.regions, bool(V.gates[0, h]))[i]).tolist())
+                forced.add(tb[0])
+                cand = [j for j in range(nv) if j not in forced]
+                best = sorted(cand, key=lambda j: (-keys[i, j], j))[:max(0, kk - len(forced))]
+                assert video == sorted((forced | set(best)) - set(tb))
+
+
+def test_text_blocks_layout():
+    assert list(O.text_blocks(256, 256, 32)) == []
+    assert list(O.text_blocks(256, 320, 32)) == [8, 9]          # aligned: text from block 8
+    assert list(O.text_blocks(250, 300, 32)) == [7, 8, 9]       # block 7 holds video and text
+
+
 # ------------------------------------------- Eq. 2 / Eq. 5 attention statistic
 
 @pytest.mark.parametrize("seed", range(3))

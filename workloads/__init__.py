@@ -72,14 +72,23 @@ class LayerConfig:
     block: int
     seed: int
     head_types: tuple = field(default=())   # empty: seeded 1/3 each
+    text_tokens: int = 0                    # text segment appended after the video
 
     @property
     def frame_tokens(self) -> int:
         return self.hs * self.ws
 
     @property
-    def L(self) -> int:
+    def L_video(self) -> int:
         return self.frames * self.frame_tokens
+
+    @property
+    def L(self) -> int:
+        return self.L_video + self.text_tokens
+
+    @property
+    def n_video(self) -> int:
+        return -(-self.L_video // self.block)
 
     @property
     def n(self) -> int:
@@ -104,7 +113,14 @@ CONFIGS = {
 def with_heads(cfg: LayerConfig, H: int, name: str | None = None) -> LayerConfig:
     """The same layer with H heads (heads keep their seeds and types)."""
     return LayerConfig(name or cfg.name, cfg.B, H, cfg.d, cfg.frames, cfg.hs, cfg.ws,
-                       cfg.block, cfg.seed, cfg.head_types)
+                       cfg.block, cfg.seed, cfg.head_types, cfg.text_tokens)
+
+
+def with_text(cfg: LayerConfig, text_tokens: int, name: str | None = None) -> LayerConfig:
+    """The same layer with a text segment of `text_tokens` tokens appended
+    after the video tokens (the video part is drawn identically)."""
+    return LayerConfig(name or f"{cfg.name}+text{text_tokens}", cfg.B, cfg.H, cfg.d, cfg.frames,
+                       cfg.hs, cfg.ws, cfg.block, cfg.seed, cfg.head_types, text_tokens)
 
 
 # ----------------------------------------------------------------------------
@@ -190,7 +206,7 @@ def _draw_head(cfg: LayerConfig, b: int, h: int, htype: int, axes, seed: int | N
     the per-axis features; phi R is formed as the sum of the three axis
     blocks times the matching rows of R (same product, fewer flops)."""
     rng = _head_rng(cfg.seed if seed is None else seed, b, h)
-    d, L = cfg.d, cfg.L
+    d, L = cfg.d, cfg.L_video
     R, _ = np.linalg.qr(rng.standard_normal((d, d)))
     ft, fy, fx = axes
     dt, ds = ft.shape[1], fy.shape[1]
@@ -209,7 +225,7 @@ def _draw_head(cfg: LayerConfig, b: int, h: int, htype: int, axes, seed: int | N
         # attention sinks: half the tokens of ~2% of the key blocks
         g = rng.standard_normal(d)
         g = (g / np.linalg.norm(g)).astype(np.float32)
-        bs, n = cfg.block, cfg.n
+        bs, n = cfg.block, cfg.n_video
         sinks = np.sort(rng.choice(n, size=max(1, int(round(_SINK_BLOCK_FRACTION * n))),
                                    replace=False))
         idx = []
@@ -220,6 +236,16 @@ def _draw_head(cfg: LayerConfig, b: int, h: int, htype: int, axes, seed: int | N
         amp = math.sqrt(_ANCHOR_LOGIT * math.sqrt(d))   # alpha = beta, alpha*beta/sqrt(d) = boost
         q += np.float32(amp) * g[None, :]
         k[idx] += np.float32(amp) * g[None, :]
+    if cfg.text_tokens:
+        # text tokens: unstructured features at the video tokens' RMS, from a
+        # stream of their own (the video part does not depend on them)
+        trng = _head_rng(cfg.seed if seed is None else seed, b, h, tag=2)
+        T = cfg.text_tokens
+        rms = float(np.sqrt(np.mean(base * base) + _NOISE_WEIGHT ** 2))
+        tq = rms * trng.standard_normal((T, d), dtype=np.float32)
+        tk = rms * trng.standard_normal((T, d), dtype=np.float32)
+        tv = trng.standard_normal((T, d), dtype=np.float32)
+        q, k, v = (np.concatenate([a, t]) for a, t in ((q, tq), (k, tk), (v, tv)))
     return q, k, v
 
 
