@@ -27,8 +27,17 @@
  *     block may be short (n = ceil(L / block) blocks).
  *   - Tokens are frame-first; `frame_tokens` tokens make one latent frame and
  *     each frame defines one block-diagonal region (Appendix B.3).
- *   - Supported: d in {64, 128}, block in {64, 128}, 2 <= L / frame_tokens,
- *     L % frame_tokens == 0, n <= 4096.  Other shapes: MOD_ERR_UNSUPPORTED.
+ *   - Token-type-aware masking (Section 3): the last `text_tokens` tokens of
+ *     the sequence may be text tokens that attend to, and are attended by,
+ *     every token.  The MOD statistic, fit and prediction cover the
+ *     Lv = L - text_tokens video tokens (nv = ceil(Lv / block) blocks); the
+ *     masks cover all n blocks.  A block holding any text token is a text
+ *     block (the first is Lv / block): its row keeps every block, and every
+ *     row keeps it.  In a block holding both video and text tokens (Lv not a
+ *     multiple of block) the video part is pooled with the video tokens.
+ *   - Supported: d in {64, 128}, block in {64, 128}, 0 <= text_tokens < L,
+ *     2 <= Lv / frame_tokens, Lv % frame_tokens == 0, n <= 4096.  Other
+ *     shapes: MOD_ERR_UNSUPPORTED.
  *   - Every call is asynchronous on `stream` (a hipStream_t; NULL is the
  *     default stream) unless stated otherwise.  Arguments are validated on
  *     the host before anything is enqueued; on error nothing is enqueued and
@@ -63,6 +72,7 @@ typedef struct {
     int d;             /* head dimension                         */
     int block;         /* tokens per block (the paper's B)       */
     int frame_tokens;  /* tokens per latent frame                */
+    int text_tokens;   /* text tokens after the video (0: none)  */
 } mod_shape;
 
 /* Predictor schedule (Algorithm 1 hyper-parameters). */
@@ -103,16 +113,18 @@ typedef struct {
     int mode;          /* mod_budget_mode              */
     float density;     /* TOPK: in (0, 1]              */
     float mass;        /* MASS: in (0, 1]              */
-    int patterns;      /* PATTERN: K in [1, 3n - 1]    */
+    int patterns;      /* PATTERN: K in [1, 3nv - 1]   */
 } mod_budget;
 
 typedef struct mod_stats mod_stats;   /* opaque, library-owned */
 
-/* n = ceil(L / block); 0 for a null or invalid shape. */
+/* n = ceil(L / block), the blocks of the whole sequence (the masks' size);
+ * 0 for a null or invalid shape. */
 int mod_num_blocks(const mod_shape* shape);
 
-/* |X| = 3n - 1 + F coefficients per head (Eq. 4: 2n-1 diagonals, n
- * verticals, F = L / frame_tokens frame regions); 0 if invalid. */
+/* |X| = 3nv - 1 + F coefficients per head (Eq. 4: 2nv-1 diagonals, nv
+ * verticals, F = Lv / frame_tokens frame regions, over the nv video
+ * blocks); 0 if invalid. */
 int mod_num_coeffs(const mod_shape* shape);
 
 /* Create the predictor state of one layer.  Builds, on the host in fp64, the
@@ -147,7 +159,9 @@ mod_status mod_collect_stats(mod_stats* stats, const void* q, const void* k, int
  * replaces the stored value; unlisted blocks keep their previous value
  * (Eq. 5 at block level).  The MOD model is then fitted to the whole stored
  * map and (step, X) becomes the newest anchor.  The first update should
- * list every block (the stored map starts at zero).
+ * list every block (the stored map starts at zero).  With text tokens the
+ * map covers the video blocks (i, j < nv) while the lists, the lse and the
+ * probabilities cover the whole sequence.
  * q, k: [B,H,L,d] bf16 device (the step's inputs, scaled as in the
  * attention call: scale = 1/sqrt(d)); lse: [B,H,L] fp32 device, the lse the
  * attention forward returned for these lists; kv_idx, kv_cnt: the lists of
@@ -166,9 +180,12 @@ mod_status mod_update_stats(mod_stats* stats, const void* q, const void* k, cons
  * come from mod_update_stats only and q, k are never read.  Then c and d are extrapolated to `step`
  * from the two newest anchors (zero slope with one anchor) and every query
  * block i of every head selects key blocks by the score
- *   sigma(i, j) = n * (c~[j - i] + d~[j])
+ *   sigma(i, j) = nv * (c~[j - i] + d~[j])
  * ranked at float precision, ties to the smaller j, the frame blocks of i
- * forced in when the gate is on.
+ * forced in when the gate is on (and the block holding both video and text
+ * tokens, if any).  TOPK counts k over the nv video blocks.  With text
+ * tokens every video row then keeps the text blocks, and the rows of the
+ * text blocks keep every block.
  * Output (device, caller-owned):
  *   kv_idx [B, H, n, n] int32: row (b,h,i) starts at ((b*H+h)*n+i)*n and
  *          holds kv_cnt[(b*H+h)*n+i] ascending block indices; the rest of
@@ -190,8 +207,8 @@ size_t mod_attn_workspace_bytes(const mod_shape* shape);
  * mod_predict_block_mask; indices in [0, n), each at most once).  A row with
  * kv_cnt = 0 gives O = 0 and lse = -inf.  scale = 0 means 1/sqrt(d).
  * q, k, v, o: [B,H,L,d] bf16 device; lse: [B,H,L] fp32 device or NULL.
- * bf16 MFMA products, fp32 softmax and accumulation.  `frame_tokens` of the
- * shape is not used.  workspace may be NULL when mod_attn_workspace_bytes
+ * bf16 MFMA products, fp32 softmax and accumulation.  `frame_tokens` and
+ * `text_tokens` of the shape are not used.  workspace may be NULL when mod_attn_workspace_bytes
  * returns 0. */
 mod_status mod_block_sparse_attn_fwd(const mod_shape* shape, const void* q, const void* k,
                                      const void* v, const int32_t* kv_idx,
@@ -200,20 +217,22 @@ mod_status mod_block_sparse_attn_fwd(const mod_shape* shape, const void* q, cons
 
 /* ---- introspection (synchronous copies to host memory; for tests) ---- */
 
+/* The sizes below count the nv video blocks (nv = n without text tokens). */
+
 /* Anchor `slot` (0 = newest, 1 = the one before): coefficients
- * [B, H, 3n-1+F] fp64 (order c_{-(n-1)..n-1}, d_{0..n-1}, e_{0..F-1};
+ * [B, H, 3nv-1+F] fp64 (order c_{-(nv-1)..nv-1}, d_{0..nv-1}, e_{0..F-1};
  * minimum-norm gauge) and its step.  MOD_ERR_BAD_STATE if absent. */
 mod_status mod_stats_get_anchor(const mod_stats* stats, int slot, double* host_coeffs,
                                 int* step);
 
-/* Block means of the last fitted q, k: [B, H, n, d] fp64 each. */
+/* Block means of the last fitted q, k: [B, H, nv, d] fp64 each. */
 mod_status mod_stats_get_pooled(const mod_stats* stats, double* host_qbar, double* host_kbar);
 
-/* The fitted statistic of the last fit: [B, H, n, n] fp64 (statistic 0: the
+/* The fitted statistic of the last fit: [B, H, nv, nv] fp64 (statistic 0: the
  * pooled block mass G; statistic 1: the stored informativeness map I). */
 mod_status mod_stats_get_block_mass(const mod_stats* stats, double* host_G);
 
-/* Last prediction (c~, d~): [B, H, 3n-1] fp64. */
+/* Last prediction (c~, d~): [B, H, 3nv-1] fp64. */
 mod_status mod_stats_get_prediction(const mod_stats* stats, double* host_pred);
 
 /* Block-diagonal gate per head, [B, H] int32 (0/1); MOD_ERR_BAD_STATE

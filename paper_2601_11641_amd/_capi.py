@@ -36,7 +36,7 @@ class ModError(RuntimeError):
 
 class mod_shape(ctypes.Structure):
     _fields_ = [("B", c_int), ("H", c_int), ("L", c_int), ("d", c_int), ("block", c_int),
-                ("frame_tokens", c_int)]
+                ("frame_tokens", c_int), ("text_tokens", c_int)]
 
 
 class mod_params(ctypes.Structure):
@@ -124,8 +124,14 @@ def _stream(stream):
     return torch.cuda.current_stream().cuda_stream
 
 
-def make_shape(B, H, L, d, block, frame_tokens=0) -> mod_shape:
-    return mod_shape(B, H, L, d, block, frame_tokens)
+def make_shape(B, H, L, d, block, frame_tokens=0, text_tokens=0) -> mod_shape:
+    return mod_shape(B, H, L, d, block, frame_tokens, text_tokens)
+
+
+def num_video_blocks(shape: mod_shape) -> int:
+    """nv: the blocks of the video tokens, over which the MOD model and the
+    introspection arrays are sized."""
+    return -(-(shape.L - shape.text_tokens) // shape.block)
 
 
 def make_params(warmup_m=1, delta_t=0, tau_e=0.0, anchor_rule=0, statistic=0, eta=1e-4) -> mod_params:
@@ -257,6 +263,7 @@ class Stats:
         self.shape, self.params = shape, params
         self.handle = mod_stats_create(shape, params)
         self.n = mod_num_blocks(shape)
+        self.n_video = num_video_blocks(shape)
         self.p = mod_num_coeffs(shape)
 
     def close(self):

@@ -535,12 +535,16 @@ hipError_t launch(const uint16_t* q, const uint16_t* k, const uint16_t* v, const
 // rows; the K tiles of the row's list are copied into LDS one tile ahead.
 // The result is written into stat[bh][i][j] (fp64); blocks not listed keep
 // their previous value (the reconstruction of Eq. 5).
+// With a text segment after the video the lists cover all n blocks of the
+// sequence while the statistic covers the first nv (video) blocks: rows
+// i < nv are counted and only entries j < nv are stored (stat [BH, nv, nv]).
 // ---------------------------------------------------------------------------
 template <int D, int BS>
 __global__ __launch_bounds__(BS * 2, 1) void stat_count_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const int32_t* __restrict__ kv_idx, const int32_t* __restrict__ kv_cnt,
-    const float* __restrict__ lse, float scale, float log_eta, double* __restrict__ stat, int L, int n) {
+    const float* __restrict__ lse, float scale, float log_eta, double* __restrict__ stat, int L, int n,
+    int nv) {
     constexpr int QW = BS / 32;        // waves, 32 query rows each
     constexpr int RT = BS / 32;        // 32-row kv sub-tiles per tile
     constexpr int KK = D / 16;
@@ -551,8 +555,8 @@ __global__ __launch_bounds__(BS * 2, 1) void stat_count_kernel(
     __shared__ __align__(1024) char kb1[TILE];
     __shared__ int part[2][QW];
 
-    const int item = blockIdx.x;       // bh * n + i
-    const int bh = item / n, i = item % n;
+    const int bh = blockIdx.x / nv, i = blockIdx.x % nv;
+    const size_t item = (size_t)bh * n + i;    // row of the lists
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int h = lane >> 5, l32 = lane & 31;
@@ -610,11 +614,11 @@ __global__ __launch_bounds__(BS * 2, 1) void stat_count_kernel(
         if (lane == 0) part[t & 1][w] = c;
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
-        if (tid == 0 && j >= 0) {
+        if (tid == 0 && j >= 0 && j < nv) {
             int total = 0;
 #pragma unroll
             for (int ww = 0; ww < QW; ++ww) total += part[t & 1][ww];
-            stat[(size_t)item * n + j] = (double)total / ((double)rows_i * (double)kvalid);
+            stat[((size_t)bh * nv + i) * nv + j] = (double)total / ((double)rows_i * (double)kvalid);
         }
     }
 }
@@ -622,9 +626,9 @@ __global__ __launch_bounds__(BS * 2, 1) void stat_count_kernel(
 template <int D, int BS>
 hipError_t launch_count(const uint16_t* q, const uint16_t* k, const int32_t* kv_idx, const int32_t* kv_cnt,
                         const float* lse, float scale, float log_eta, double* stat, int BH, int L, int n,
-                        hipStream_t s) {
-    hipLaunchKernelGGL((stat_count_kernel<D, BS>), dim3((unsigned)BH * n), dim3(BS * 2), 0, s, q, k, kv_idx,
-                       kv_cnt, lse, scale, log_eta, stat, L, n);
+                        int nv, hipStream_t s) {
+    hipLaunchKernelGGL((stat_count_kernel<D, BS>), dim3((unsigned)BH * nv), dim3(BS * 2), 0, s, q, k, kv_idx,
+                       kv_cnt, lse, scale, log_eta, stat, L, n, nv);
     return hipGetLastError();
 }
 
@@ -642,11 +646,11 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
 
 hipError_t launch_stat_count(const uint16_t* q, const uint16_t* k, const int32_t* kv_idx,
                              const int32_t* kv_cnt, const float* lse, float scale, float log_eta,
-                             double* stat, int BH, int L, int d, int bs, int n, hipStream_t s) {
-    if (d == 128 && bs == 128) return launch_count<128, 128>(q, k, kv_idx, kv_cnt, lse, scale, log_eta, stat, BH, L, n, s);
-    if (d == 128 && bs == 64) return launch_count<128, 64>(q, k, kv_idx, kv_cnt, lse, scale, log_eta, stat, BH, L, n, s);
-    if (d == 64 && bs == 128) return launch_count<64, 128>(q, k, kv_idx, kv_cnt, lse, scale, log_eta, stat, BH, L, n, s);
-    return launch_count<64, 64>(q, k, kv_idx, kv_cnt, lse, scale, log_eta, stat, BH, L, n, s);
+                             double* stat, int BH, int L, int d, int bs, int n, int nv, hipStream_t s) {
+    if (d == 128 && bs == 128) return launch_count<128, 128>(q, k, kv_idx, kv_cnt, lse, scale, log_eta, stat, BH, L, n, nv, s);
+    if (d == 128 && bs == 64) return launch_count<128, 64>(q, k, kv_idx, kv_cnt, lse, scale, log_eta, stat, BH, L, n, nv, s);
+    if (d == 64 && bs == 128) return launch_count<64, 128>(q, k, kv_idx, kv_cnt, lse, scale, log_eta, stat, BH, L, n, nv, s);
+    return launch_count<64, 64>(q, k, kv_idx, kv_cnt, lse, scale, log_eta, stat, BH, L, n, nv, s);
 }
 
 }  // namespace moddit

@@ -50,11 +50,14 @@ mod_status check_shape(const mod_shape* s, bool need_frames) {
         return fail(MOD_ERR_UNSUPPORTED, "B*H*n too large");
     if (need_frames) {
         if (s->frame_tokens <= 0) return fail(MOD_ERR_INVALID_ARG, "frame_tokens must be positive");
-        if (s->L % s->frame_tokens != 0)
-            return fail(MOD_ERR_UNSUPPORTED, "L=%d is not a whole number of frames of %d tokens", s->L,
-                        s->frame_tokens);
-        if (s->L / s->frame_tokens < 2)
-            return fail(MOD_ERR_UNSUPPORTED, "need at least 2 frames (F=%d)", s->L / s->frame_tokens);
+        if (s->text_tokens < 0 || s->text_tokens >= s->L)
+            return fail(MOD_ERR_INVALID_ARG, "text_tokens=%d must be in [0, L)", s->text_tokens);
+        const int Lv = s->L - s->text_tokens;
+        if (Lv % s->frame_tokens != 0)
+            return fail(MOD_ERR_UNSUPPORTED, "%d video tokens are not a whole number of frames of %d tokens",
+                        Lv, s->frame_tokens);
+        if (Lv / s->frame_tokens < 2)
+            return fail(MOD_ERR_UNSUPPORTED, "need at least 2 frames (F=%d)", Lv / s->frame_tokens);
     }
     return MOD_OK;
 }
@@ -177,7 +180,10 @@ bool build_schur_inverse(int n, const std::vector<int>& lo, const std::vector<in
 struct mod_stats {
     mod_shape shape{};
     mod_params params{};
-    int n = 0, F = 0, p = 0, q = 0, BH = 0;
+    int n = 0, F = 0, p = 0, q = 0, BH = 0;   // n: video blocks (the MOD model's)
+    int Lv = 0;                // video tokens
+    int nt = 0;                // blocks of the whole sequence (the masks')
+    int tb0 = 0;               // first text block (nt without text)
     double scale = 0.0;
     int device = 0;
     // device buffers
@@ -244,9 +250,9 @@ mod_status fit_into_next_slot(mod_stats* s, const void* q, const void* k, int st
                               hipStream_t st) {
     const mod_shape& sh = s->shape;
     hipError_t e = moddit::launch_pool(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-                                       s->qbar, s->kbar, s->BH, sh.L, sh.d, sh.block, s->n, st);
+                                       s->qbar, s->kbar, s->BH, s->Lv, sh.L, sh.d, sh.block, s->n, st);
     if (e != hipSuccess) return hip_fail(e, "pool launch");
-    e = moddit::launch_block_mass(s->qbar, s->kbar, s->G, s->BH, sh.L, sh.d, sh.block, s->n, s->scale, st);
+    e = moddit::launch_block_mass(s->qbar, s->kbar, s->G, s->BH, s->Lv, sh.d, sh.block, s->n, s->scale, st);
     if (e != hipSuccess) return hip_fail(e, "block-mass launch");
     return fit_stat_into_next_slot(s, step, st);
 }
@@ -274,9 +280,12 @@ int mod_num_blocks(const mod_shape* shape) {
 }
 
 int mod_num_coeffs(const mod_shape* shape) {
-    const int n = mod_num_blocks(shape);
-    if (n == 0 || shape->frame_tokens <= 0 || shape->L % shape->frame_tokens) return 0;
-    return 3 * n - 1 + shape->L / shape->frame_tokens;
+    if (mod_num_blocks(shape) == 0 || shape->frame_tokens <= 0 || shape->text_tokens < 0 ||
+        shape->text_tokens >= shape->L)
+        return 0;
+    const int Lv = shape->L - shape->text_tokens;
+    if (Lv % shape->frame_tokens) return 0;
+    return 3 * ceil_div(Lv, shape->block) - 1 + Lv / shape->frame_tokens;
 }
 
 mod_status mod_stats_create(const mod_shape* shape, const mod_params* params, mod_stats** out) {
@@ -298,8 +307,11 @@ mod_status mod_stats_create(const mod_shape* shape, const mod_params* params, mo
     if (!s) return fail(MOD_ERR_NOMEM, "host allocation failed");
     s->shape = *shape;
     s->params = *params;
-    s->n = ceil_div(shape->L, shape->block);
-    s->F = shape->L / shape->frame_tokens;
+    s->Lv = shape->L - shape->text_tokens;
+    s->n = ceil_div(s->Lv, shape->block);
+    s->nt = ceil_div(shape->L, shape->block);
+    s->tb0 = shape->text_tokens > 0 ? s->Lv / shape->block : s->nt;
+    s->F = s->Lv / shape->frame_tokens;
     s->p = 3 * s->n - 1 + s->F;
     s->q = s->n - 1 + s->F;
     s->BH = shape->B * shape->H;
@@ -402,7 +414,7 @@ mod_status mod_update_stats(mod_stats* s, const void* q, const void* k, const fl
     hipError_t e = moddit::launch_stat_count(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                                              kv_idx, kv_cnt, lse, (float)s->scale,
                                              (float)std::log((double)s->params.eta), s->G, s->BH, sh.L, sh.d,
-                                             sh.block, s->n, hs);
+                                             sh.block, s->nt, s->n, hs);
     if (e != hipSuccess) return hip_fail(e, "statistic launch");
     st = fit_stat_into_next_slot(s, step, hs);
     if (st != MOD_OK) return st;
@@ -467,10 +479,10 @@ mod_status mod_predict_block_mask(mod_stats* s, const void* q, const void* k, in
     if (e != hipSuccess) return hip_fail(e, "extrapolate launch");
     if (budget->mode == MOD_BUDGET_PATTERN)
         e = moddit::launch_select_patterns(s->pred, s->gate, s->row_lo, s->row_hi, budget->patterns,
-                                           s->chosen, kv_idx, kv_cnt, s->BH, n, hs);
+                                           s->chosen, kv_idx, kv_cnt, s->BH, n, s->nt, s->tb0, hs);
     else
         e = moddit::launch_select(s->pred, s->gate, s->row_lo, s->row_hi, budget->mode, topk, tau,
-                                  kv_idx, kv_cnt, s->BH, n, hs);
+                                  kv_idx, kv_cnt, s->BH, n, s->nt, s->tb0, hs);
     if (e != hipSuccess) return hip_fail(e, "select launch");
     s->has_step = true;
     s->last_step = step;

@@ -12,9 +12,10 @@ namespace moddit {
 
 constexpr int kMaxBlocks = 4096;     // largest n (selection keeps a row in LDS)
 
-// a1: block means of Q and K, fp64 [BH, n, d].
+// a1: block means of Q and K, fp64 [BH, n, d], over the first L tokens of
+// each head (L_stride tokens apart).
 hipError_t launch_pool(const uint16_t* q, const uint16_t* k, double* qbar, double* kbar,
-                       int BH, int L, int d, int bs, int n, hipStream_t s);
+                       int BH, int L, int L_stride, int d, int bs, int n, hipStream_t s);
 
 // a2: pooled block-mass statistic G [BH, n, n] fp64 (row-stochastic).
 hipError_t launch_block_mass(const double* qbar, const double* kbar, double* G, int BH,
@@ -38,16 +39,19 @@ hipError_t launch_extrapolate(const double* X1, const double* X2, double w, doub
 
 // a5: per-row selection into compacted lists.  row_lo/row_hi: union of the
 // frame regions holding block i; mode 0 = TOPK (k), 1 = MASS (tau).
+// n: video blocks; ldn >= n: blocks of the whole sequence (lists
+// [BH, ldn, ldn]); tb0: first text block (ldn when there is no text).  The
+// text blocks are kept in every row and the text rows keep every block.
 hipError_t launch_select(const double* pred, const int32_t* gate, const int* row_lo,
                          const int* row_hi, int mode, int k, double tau, int32_t* kv_idx,
-                         int32_t* kv_cnt, int BH, int n, hipStream_t s);
+                         int32_t* kv_cnt, int BH, int n, int ldn, int tb0, hipStream_t s);
 
 // a5, pattern form: the K largest pattern intensities per head (chosen
 // [BH, 3n-1] bytes, scratch), then per-row lists of the blocks a chosen
 // diagonal or column covers, plus the forced blocks.
 hipError_t launch_select_patterns(const double* pred, const int32_t* gate, const int* row_lo,
                                   const int* row_hi, int K, uint8_t* chosen, int32_t* kv_idx,
-                                  int32_t* kv_cnt, int BH, int n, hipStream_t s);
+                                  int32_t* kv_cnt, int BH, int n, int ldn, int tb0, hipStream_t s);
 
 // a6: block-sparse attention forward.
 hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v,
@@ -58,9 +62,10 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
 // Eq. 2 statistic of a computed attention map: stat[bh][i][j] = fraction of
 // the probabilities of listed block (i, j) that reach exp(log_eta), with the
 // row LSE of the attention forward over the same lists; unlisted blocks keep
-// their value.
+// their value.  Lists over the n blocks of the sequence; stat [BH, nv, nv]
+// over its first nv (video) blocks.
 hipError_t launch_stat_count(const uint16_t* q, const uint16_t* k, const int32_t* kv_idx,
                              const int32_t* kv_cnt, const float* lse, float scale, float log_eta,
-                             double* stat, int BH, int L, int d, int bs, int n, hipStream_t s);
+                             double* stat, int BH, int L, int d, int bs, int n, int nv, hipStream_t s);
 
 }  // namespace moddit

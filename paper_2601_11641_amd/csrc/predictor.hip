@@ -53,18 +53,19 @@ __device__ double block_max(double v, double* red) {
 // a1: block pooling.  Grid (n, BH, 2): z = 0 pools Q, z = 1 pools K.  The
 // block is one contiguous run of rows*D bf16; each thread reads 16-byte
 // chunks of a fixed channel group on every R-th row and accumulates in fp64.
+// L: tokens pooled (the video tokens); L_stride: tokens per head in memory.
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(kThreads) void pool_kernel(const uint16_t* __restrict__ q,
                                                         const uint16_t* __restrict__ k,
                                                         double* __restrict__ qbar,
                                                         double* __restrict__ kbar, int L,
-                                                        int bs, int n) {
+                                                        int L_stride, int bs, int n) {
     constexpr int C = D / 8;        // 16-byte chunks per row
     constexpr int R = kThreads / C; // rows per pass
     __shared__ double part[R][D + 1];
     const int i = blockIdx.x, bh = blockIdx.y;
-    const uint16_t* src = (blockIdx.z == 0 ? q : k) + ((size_t)bh * L + (size_t)i * bs) * D;
+    const uint16_t* src = (blockIdx.z == 0 ? q : k) + ((size_t)bh * L_stride + (size_t)i * bs) * D;
     double* dst = (blockIdx.z == 0 ? qbar : kbar) + ((size_t)bh * n + i) * D;
     const int cnt = min(bs, L - i * bs);
     const int t = threadIdx.x, c = t % C, r0 = t / C;
@@ -353,6 +354,10 @@ __global__ __launch_bounds__(kThreads) void extrapolate_kernel(const double* __r
 //   shortest prefix whose positive key mass, added to the forced blocks'
 //   mass, reaches tau of the row total (fp64 prefix sums; at least one block).
 //   The kept set is compacted in ascending j.
+// With a text segment after the video (token-type-aware masking) n counts
+// the video blocks, the lists have ldn >= n entries per row, the block tb0
+// shared by the video and the text (tb0 < n) is forced, and every row keeps
+// the text blocks n .. ldn-1 after its video selection.  tb0 >= ldn: none.
 // ---------------------------------------------------------------------------
 __device__ inline uint32_t order_bits(float f) {
     const uint32_t u = __float_as_uint(f);
@@ -367,7 +372,8 @@ __device__ inline float order_bits_to_float(uint32_t k) {
 __global__ __launch_bounds__(kThreads) void select_kernel(
     const double* __restrict__ pred, const int32_t* __restrict__ gate,
     const int* __restrict__ row_lo, const int* __restrict__ row_hi, int mode, int topk,
-    double tau, int32_t* __restrict__ kv_idx, int32_t* __restrict__ kv_cnt, int n, int npad) {
+    double tau, int32_t* __restrict__ kv_idx, int32_t* __restrict__ kv_cnt, int n, int npad,
+    int ldn, int tb0) {
     extern __shared__ __align__(16) unsigned char smem[];
     uint64_t* keys = reinterpret_cast<uint64_t*>(smem);          // npad
     double* scan = reinterpret_cast<double*>(keys + npad);        // npad
@@ -382,7 +388,10 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     const double* d = c + (2 * n - 1);
     const bool g = gate[bh] != 0;
     const int flo = row_lo[i], fhi = row_hi[i];
-    const int nf = g ? (fhi - flo + 1) : 0;
+    // forced: the frame blocks of i (gate on) and the block shared by the
+    // video and the text segment (tb0 < n), which is a text block
+    const bool tb_in_frames = g && tb0 >= flo && tb0 <= fhi;
+    const int nf = (g ? (fhi - flo + 1) : 0) + ((tb0 < n && !tb_in_frames) ? 1 : 0);
     const int n_free = n - nf;
     const int t = threadIdx.x;
 
@@ -393,7 +402,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
         if (j < n) {
             const double s = static_cast<double>(n) * (c[j - i + n - 1] + d[j]);
             const float kf = static_cast<float>(s);
-            if (g && j >= flo && j <= fhi) {
+            if ((g && j >= flo && j <= fhi) || j == tb0) {
                 fl = 1;
                 forced_mass += fmax(static_cast<double>(kf), 0.0);
             } else {
@@ -488,15 +497,20 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
             ired[a] = off;
             off += v;
         }
-        kv_cnt[row] = off;
+        kk_shared = off;
     }
     __syncthreads();
+    const int total = kk_shared;
+    const size_t orow = (size_t)bh * ldn + i;     // row of the [BH, ldn, ldn] lists
     int pos = ired[t];
-    int32_t* out = kv_idx + (size_t)row * n;
+    int32_t* out = kv_idx + orow * ldn;
     for (int e = 0; e < E; ++e) {
         const int j = t * E + e;
         if (flag[j]) out[pos++] = j;
     }
+    // text blocks after the video blocks: kept in every row
+    for (int j = n + t; j < ldn; j += kThreads) out[total + (j - n)] = j;
+    if (t == 0) kv_cnt[orow] = total + (ldn - n);
 }
 
 inline unsigned cdiv(long a, long b) { return static_cast<unsigned>((a + b - 1) / b); }
@@ -563,7 +577,7 @@ __global__ __launch_bounds__(kThreads) void pattern_rank_kernel(const double* __
 __global__ __launch_bounds__(kThreads) void pattern_rows_kernel(
     const uint8_t* __restrict__ chosen, const int32_t* __restrict__ gate,
     const int* __restrict__ row_lo, const int* __restrict__ row_hi, int32_t* __restrict__ kv_idx,
-    int32_t* __restrict__ kv_cnt, int n) {
+    int32_t* __restrict__ kv_cnt, int n, int ldn, int tb0) {
     __shared__ int wtot[kThreads / 64];
     constexpr int JPT = kMaxBlocks / kThreads;
     const int row = blockIdx.x;
@@ -577,7 +591,8 @@ __global__ __launch_bounds__(kThreads) void pattern_rows_kernel(
 #pragma unroll
     for (int e = 0; e < JPT; ++e) {
         const int j = t * JPT + e;
-        keep[e] = j < n && (ch[j - i + n - 1] || ch[2 * n - 1 + j] || (g && j >= flo && j <= fhi));
+        keep[e] = j < n && (ch[j - i + n - 1] || ch[2 * n - 1 + j] || (g && j >= flo && j <= fhi) ||
+                            j == tb0);
         mine += keep[e] ? 1 : 0;
     }
     int incl = mine;
@@ -594,20 +609,34 @@ __global__ __launch_bounds__(kThreads) void pattern_rows_kernel(
         pos += ww < w ? wtot[ww] : 0;
         total += wtot[ww];
     }
-    int32_t* out = kv_idx + (size_t)row * n;
+    const size_t orow = (size_t)bh * ldn + i;     // row of the [BH, ldn, ldn] lists
+    int32_t* out = kv_idx + orow * ldn;
 #pragma unroll
     for (int e = 0; e < JPT; ++e)
         if (keep[e]) out[pos++] = t * JPT + e;
-    if (t == 0) kv_cnt[row] = total;
+    // text blocks after the video blocks: kept in every row
+    for (int j = n + t; j < ldn; j += kThreads) out[total + (j - n)] = j;
+    if (t == 0) kv_cnt[orow] = total + (ldn - n);
+}
+
+// Token-type-aware masking: the rows of the blocks holding text tokens
+// (tb0 .. ldn-1) keep every block.  Grid (ldn - tb0, BH).
+__global__ __launch_bounds__(kThreads) void text_rows_kernel(int32_t* __restrict__ kv_idx,
+                                                             int32_t* __restrict__ kv_cnt, int ldn,
+                                                             int tb0) {
+    const size_t orow = (size_t)blockIdx.y * ldn + tb0 + blockIdx.x;
+    int32_t* out = kv_idx + orow * ldn;
+    for (int j = threadIdx.x; j < ldn; j += kThreads) out[j] = j;
+    if (threadIdx.x == 0) kv_cnt[orow] = ldn;
 }
 
 hipError_t launch_pool(const uint16_t* q, const uint16_t* k, double* qbar, double* kbar,
-                       int BH, int L, int d, int bs, int n, hipStream_t s) {
+                       int BH, int L, int L_stride, int d, int bs, int n, hipStream_t s) {
     const dim3 grid(n, BH, 2);
     if (d == 128)
-        hipLaunchKernelGGL(pool_kernel<128>, grid, dim3(kThreads), 0, s, q, k, qbar, kbar, L, bs, n);
+        hipLaunchKernelGGL(pool_kernel<128>, grid, dim3(kThreads), 0, s, q, k, qbar, kbar, L, L_stride, bs, n);
     else
-        hipLaunchKernelGGL(pool_kernel<64>, grid, dim3(kThreads), 0, s, q, k, qbar, kbar, L, bs, n);
+        hipLaunchKernelGGL(pool_kernel<64>, grid, dim3(kThreads), 0, s, q, k, qbar, kbar, L, L_stride, bs, n);
     return hipGetLastError();
 }
 
@@ -663,9 +692,16 @@ hipError_t launch_extrapolate(const double* X1, const double* X2, double w, doub
     return hipGetLastError();
 }
 
+hipError_t launch_text_rows(int32_t* kv_idx, int32_t* kv_cnt, int BH, int ldn, int tb0, hipStream_t s) {
+    if (tb0 >= ldn) return hipSuccess;
+    hipLaunchKernelGGL(text_rows_kernel, dim3((unsigned)(ldn - tb0), (unsigned)BH), dim3(kThreads), 0, s,
+                       kv_idx, kv_cnt, ldn, tb0);
+    return hipGetLastError();
+}
+
 hipError_t launch_select(const double* pred, const int32_t* gate, const int* row_lo,
                          const int* row_hi, int mode, int k, double tau, int32_t* kv_idx,
-                         int32_t* kv_cnt, int BH, int n, hipStream_t s) {
+                         int32_t* kv_cnt, int BH, int n, int ldn, int tb0, hipStream_t s) {
     int npad = kThreads;
     while (npad < n) npad <<= 1;
     const size_t lds = (size_t)npad * (sizeof(uint64_t) + sizeof(double) + sizeof(int));
@@ -678,19 +714,23 @@ hipError_t launch_select(const double* pred, const int32_t* gate, const int* row
         attr_set = true;
     }
     hipLaunchKernelGGL(select_kernel, dim3((unsigned)BH * n), dim3(kThreads), lds, s, pred, gate,
-                       row_lo, row_hi, mode, k, tau, kv_idx, kv_cnt, n, npad);
-    return hipGetLastError();
+                       row_lo, row_hi, mode, k, tau, kv_idx, kv_cnt, n, npad, ldn, tb0);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_text_rows(kv_idx, kv_cnt, BH, ldn, tb0, s);
 }
 
 hipError_t launch_select_patterns(const double* pred, const int32_t* gate, const int* row_lo,
                                   const int* row_hi, int K, uint8_t* chosen, int32_t* kv_idx,
-                                  int32_t* kv_cnt, int BH, int n, hipStream_t s) {
+                                  int32_t* kv_cnt, int BH, int n, int ldn, int tb0, hipStream_t s) {
     hipLaunchKernelGGL(pattern_rank_kernel, dim3((unsigned)BH), dim3(kThreads), 0, s, pred, chosen, n, K);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(pattern_rows_kernel, dim3((unsigned)BH * n), dim3(kThreads), 0, s, chosen, gate,
-                       row_lo, row_hi, kv_idx, kv_cnt, n);
-    return hipGetLastError();
+                       row_lo, row_hi, kv_idx, kv_cnt, n, ldn, tb0);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_text_rows(kv_idx, kv_cnt, BH, ldn, tb0, s);
 }
 
 }  // namespace moddit

@@ -49,6 +49,13 @@ def test_block_and_coefficient_counts(M):
     assert M.mod_num_blocks(s) == 591 and M.mod_num_coeffs(s) == 3 * 591 - 1 + 21
     assert M.mod_num_blocks(None) == 0
     assert M.mod_num_coeffs(M.make_shape(1, 1, 100, 64, 64, 30)) == 0
+    # a text segment: the masks count every block, the model the video ones
+    s = M.make_shape(1, 24, 118800 + 256, 128, 128, 3600, text_tokens=256)
+    assert M.mod_num_blocks(s) == 931 and M.mod_num_coeffs(s) == 3 * 929 - 1 + 33
+    assert M.num_video_blocks(s) == 929
+    s = M.make_shape(1, 2, 1000 + 100, 64, 64, 250, text_tokens=100)
+    assert M.mod_num_blocks(s) == 18 and M.mod_num_coeffs(s) == 3 * 16 - 1 + 4
+    assert M.mod_num_coeffs(M.make_shape(1, 2, 1024, 64, 64, 256, text_tokens=1024)) == 0
 
 
 @pytest.mark.parametrize("shape,status", [
@@ -59,6 +66,10 @@ def test_block_and_coefficient_counts(M):
     ((0, 2, 1024, 64, 64, 256), 1),      # empty batch
     ((1, 2, 1024, 64, 64, 0), 1),        # frame_tokens missing
     ((1, 1, 128 * 4097, 64, 128, 128), 2),  # n above the limit
+    ((1, 2, 1024 + 64, 64, 64, 256, 64 + 1), 2),   # video not whole frames
+    ((1, 2, 512 + 64, 64, 64, 256, 64 + 256), 2),  # a single video frame
+    ((1, 2, 1024, 64, 64, 256, -1), 1),            # negative text_tokens
+    ((1, 2, 1024, 64, 64, 256, 1024), 1),          # no video tokens
 ])
 def test_create_rejects_bad_shapes_on_host(M, shape, status):
     with pytest.raises(M.ModError) as e:
@@ -104,7 +115,8 @@ def test_struct_layouts_match_the_header(M, tmp_path):
         'int main(void) {\n'
         '  printf("%zu %zu %zu %zu %zu\\n", sizeof(mod_budget), offsetof(mod_budget, mode),\n'
         '         offsetof(mod_budget, density), offsetof(mod_budget, mass), offsetof(mod_budget, patterns));\n'
-        '  printf("%zu %zu\\n", sizeof(mod_shape), offsetof(mod_shape, frame_tokens));\n'
+        '  printf("%zu %zu %zu\\n", sizeof(mod_shape), offsetof(mod_shape, frame_tokens),\n'
+        '         offsetof(mod_shape, text_tokens));\n'
         '  printf("%zu %zu %zu\\n", sizeof(mod_params), offsetof(mod_params, anchor_rule),\n'
         '         offsetof(mod_params, eta));\n'
         '  return 0;\n}\n')
@@ -114,6 +126,6 @@ def test_struct_layouts_match_the_header(M, tmp_path):
     got = [int(x) for x in out]
     want = [ctypes.sizeof(M.mod_budget), M.mod_budget.mode.offset, M.mod_budget.density.offset,
             M.mod_budget.mass.offset, M.mod_budget.patterns.offset,
-            ctypes.sizeof(M.mod_shape), M.mod_shape.frame_tokens.offset,
+            ctypes.sizeof(M.mod_shape), M.mod_shape.frame_tokens.offset, M.mod_shape.text_tokens.offset,
             ctypes.sizeof(M.mod_params), M.mod_params.anchor_rule.offset, M.mod_params.eta.offset]
     assert got == want

@@ -1,0 +1,282 @@
+"""GPU parity of token-type-aware masking (Section 3): a text segment after
+the video tokens, through the C ABI, against the oracle.
+
+The MOD statistic, fit and prediction run over the video blocks; the lists
+cover every block of the sequence: the rows of the text blocks keep every
+block, every other row keeps its video selection plus the text blocks, and
+a block holding both video and text tokens is forced into the video
+selection.  Cases: a text segment that starts on a block boundary, one that
+shares a block with the last video tokens (a mixed block with a ragged video
+tail), and the attention statistic (Eq. 2 / Eq. 5) over such lists.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from parity import (GAP, LSE_ABS, MAX_ABS, MEAN_ABS, attention_errors, bf16_tensor, bf16_to_f64,
+                    compare_lists, gpu_lists)
+
+import paper_2601_11641_amd as M
+
+torch = pytest.importorskip("torch")
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+ETA = 1e-4
+TOL = 2e-4
+
+
+def _cfg(base, **kw):
+    c = W.CONFIGS[base]
+    d = dict(name=c.name, B=c.B, H=c.H, d=c.d, frames=c.frames, hs=c.hs, ws=c.ws,
+             block=c.block, seed=c.seed)
+    d.update(kw)
+    return W.LayerConfig(**d)
+
+
+CONFIGS = {
+    # 1024 video tokens (16 blocks of 64) + 40 text tokens: one text block
+    "tiny+40": W.with_text(W.CONFIGS["tiny"], 40),
+    # 8192 video tokens (64 blocks of 128) + 256 text tokens: two text blocks
+    "small3+256": W.with_text(_cfg("small", H=3), 256),
+    # 1125 video tokens (block 128: tail of 101) + 77 text tokens: block 8
+    # holds video and text tokens, block 9 text only
+    "ragged+77": W.with_text(_cfg("small", name="ragged", B=2, H=2, frames=5, hs=9, ws=25, seed=5), 77),
+}
+
+
+def _shape(cfg):
+    return M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens, cfg.text_tokens)
+
+
+def _device(cfg):
+    host = W.generate(cfg)
+    return host, tuple(bf16_tensor(x) for x in host)
+
+
+def _budgets(budget):
+    mode, val = budget
+    if mode == "topk":
+        return M.make_budget(mode, density=val), O.Budget(mode, density=val)
+    if mode == "mass":
+        return M.make_budget(mode, mass=val), O.Budget(mode, mass=val)
+    return M.make_budget(mode, patterns=val), O.Budget(mode, patterns=val)
+
+
+def _check_text_head(P, g_rows, o_rows, ct, dt_, gate_on, budget):
+    """Lists of one head: text rows full, text blocks in every row, and the
+    video part of every video row as the oracle's (up to the gap rule).
+    Returns (rows compared, rows excused)."""
+    nt, nv, tb = P.n_total, P.n, P.text
+    assert len(tb) > 0
+    for i in tb:
+        assert g_rows[i] == list(range(nt)), i
+    text_cols = set(range(tb.start, nt))
+    video_rows = [i for i in range(nt) if i not in tb]
+    for i in video_rows:
+        assert text_cols.issubset(g_rows[i]), i
+        assert g_rows[i] == sorted(set(g_rows[i])), i
+    mode = budget[0]
+    if mode == "pattern":
+        same = all(g_rows[i] == o_rows[i].kept.tolist() for i in range(nt))
+        if not same:
+            assert nv * o_rows[0].key_gap <= GAP, "pattern lists differ beyond the gap rule"
+            return nt, nt
+        return nt, 0
+    gv = [[j for j in g_rows[i] if j < nv] for i in range(nv)]
+    ov = [O.RowSelection(o_rows[i].kept[o_rows[i].kept < nv], o_rows[i].key_gap, o_rows[i].mass_margin)
+          for i in range(nv)]
+    sig = O.scores(ct, dt_, nv)
+    forced = P.forced(gate_on)
+    k = O.topk_count(budget[1], nv) if mode == "topk" else 0
+    tau = budget[1] if mode == "mass" else 1.0
+    rows = [i for i in video_rows if i < nv]
+    nr, _, nx, bad = compare_lists(gv, ov, sig, forced, mode, k, tau, rows=rows)
+    assert not bad, bad[:10]
+    return nr, nx
+
+
+def _check_attention(cfg, dev, host, rows):
+    qd, kd, vd = dev
+    o = torch.empty_like(qd)
+    lse = torch.empty((cfg.B, cfg.H, cfg.L), dtype=torch.float32, device="cuda")
+    idx, cnt = _lists_tensors(cfg, rows)
+    M.mod_block_sparse_attn_fwd(_shape(cfg), qd, kd, vd, idx, cnt, 0.0, o, lse)
+    torch.cuda.synchronize()
+    og = bf16_to_f64(o)
+    lg = lse.cpu().numpy().astype(np.float64)
+    for b in range(cfg.B):
+        for h in range(cfg.H):
+            qf, kf, vf = (W.bf16_bits_to_f64(x[b, h]) for x in host)
+            Oo, Lo = O.attention(qf, kf, vf, rows[b][h], cfg.block, 1.0 / math.sqrt(cfg.d))
+            mx, mean = attention_errors(og[b, h], Oo)
+            assert mx <= MAX_ABS and mean <= MEAN_ABS, (b, h, mx, mean)
+            assert np.abs(lg[b, h] - Lo).max() <= LSE_ABS
+
+
+def _lists_tensors(cfg, rows):
+    n = cfg.n
+    idx = torch.zeros((cfg.B, cfg.H, n, n), dtype=torch.int32)
+    cnt = torch.zeros((cfg.B, cfg.H, n), dtype=torch.int32)
+    for b in range(cfg.B):
+        for h in range(cfg.H):
+            for i, js in enumerate(rows[b][h]):
+                cnt[b, h, i] = len(js)
+                idx[b, h, i, :len(js)] = torch.tensor(js, dtype=torch.int32)
+    return idx.cuda(), cnt.cuda()
+
+
+@pytest.mark.parametrize("name", sorted(CONFIGS))
+@pytest.mark.parametrize("budget", [("topk", 0.3), ("mass", 0.8), ("pattern", 12)])
+def test_text_predictor_and_attention(name, budget):
+    cfg = CONFIGS[name]
+    host, dev = _device(cfg)
+    qd, kd, _ = dev
+    params = dict(warmup_m=2, delta_t=0, tau_e=-1.0 if budget[0] == "pattern" else 0.0)
+    st = M.Stats(_shape(cfg), M.make_params(**params))
+    B, H, nt, nv = cfg.B, cfg.H, st.n, st.n_video
+    assert (nt, nv) == (cfg.n, cfg.n_video)
+    for t in (1, 2):
+        M.mod_collect_stats(st.handle, qd, kd, t)
+    kv_idx = torch.full((B, H, nt, nt), -1, dtype=torch.int32, device="cuda")
+    kv_cnt = torch.zeros((B, H, nt), dtype=torch.int32, device="cuda")
+    gb, ob = _budgets(budget)
+    M.mod_predict_block_mask(st.handle, qd, kd, 4, gb, kv_idx, kv_cnt)
+    torch.cuda.synchronize()
+
+    qf, kf = W.bf16_bits_to_f64(host[0]), W.bf16_bits_to_f64(host[1])
+    P = O.Predictor(B, H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens, text_tokens=cfg.text_tokens, **params)
+    for t in (1, 2):
+        P.collect(qf, kf, t)
+    sel = P.predict(qf, kf, 4, ob)
+    assert (P.n, P.n_total) == (nv, nt)
+
+    # the model side sees the video tokens only
+    Lv = cfg.L_video
+    qb, kb = M.mod_stats_get_pooled(st.handle, B, H, nv, cfg.d)
+    np.testing.assert_allclose(qb, O.pool(qf[..., :Lv, :], cfg.block), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(kb, O.pool(kf[..., :Lv, :], cfg.block), rtol=1e-12, atol=1e-13)
+    G = M.mod_stats_get_block_mass(st.handle, B, H, nv)
+    np.testing.assert_allclose(G, P.pooled_mass(qf, kf), rtol=1e-10, atol=1e-15)
+    X, _ = M.mod_stats_get_anchor(st.handle, 0, B, H, st.p)
+    Xo = P.anchors[-1][1]
+    assert np.abs(X - Xo).max() <= 1e-9 * max(1.0, np.abs(Xo).max())
+    gate = M.mod_stats_get_gate(st.handle, B, H)
+    assert (gate.astype(bool) == P.gates).all()
+    pred = M.mod_stats_get_prediction(st.handle, B, H, nv)
+    po = P.prediction(4)
+
+    rows = gpu_lists(kv_idx, kv_cnt)
+    total = excused = 0
+    for b in range(B):
+        for h in range(H):
+            ct, dt_ = po[b][h]
+            ref = np.concatenate([ct, dt_])
+            assert np.abs(pred[b, h] - ref).max() <= 1e-9 * max(1.0, np.abs(ref).max())
+            nr, nx = _check_text_head(P, rows[b][h], sel[b][h], ct, dt_, bool(P.gates[b, h]), budget)
+            total, excused = total + nr, excused + nx
+    assert excused <= max(2, 0.02 * total) or budget[0] == "pattern", (excused, total)
+    _check_attention(cfg, dev, host, rows)
+    st.close()
+
+
+@pytest.mark.parametrize("name", ["ragged+77", "tiny+40"])
+def test_text_statistic_schedule(name):
+    """Statistic 1 with a text segment: dense warm-up updates at steps 1 and
+    2 (full lists over every block), predictions at 3..5 and a sparse
+    re-anchor update at step 4 from the predicted lists; the stored map
+    covers the video blocks."""
+    cfg = CONFIGS[name]
+    host, dev = _device(cfg)
+    qd, kd, _ = dev
+    params = dict(warmup_m=2, delta_t=2, tau_e=0.0)
+    st = M.Stats(_shape(cfg), M.make_params(statistic="attention", eta=ETA, **params))
+    B, H, nt, nv = cfg.B, cfg.H, st.n, st.n_video
+    P = O.Predictor(B, H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens, statistic="attention", eta=ETA,
+                    text_tokens=cfg.text_tokens, **params)
+    sizes = O.block_sizes(cfg.L, cfg.block)[:nv]
+    scale = 1.0 / math.sqrt(cfg.d)
+
+    def attention(idx, cnt):
+        o = torch.empty_like(qd)
+        lse = torch.empty((B, H, cfg.L), dtype=torch.float32, device="cuda")
+        M.mod_block_sparse_attn_fwd(_shape(cfg), qd, kd, dev[2], idx, cnt, 0.0, o, lse)
+        return lse
+
+    def check_counts(lse, rows, before, after):
+        lg = lse.cpu().numpy().astype(np.float64)
+        for b in range(B):
+            for h in range(H):
+                qf, kf = W.bf16_bits_to_f64(host[0][b, h]), W.bf16_bits_to_f64(host[1][b, h])
+                I, amb = O.attention_statistic(qf, kf, rows[b][h], cfg.block, scale, ETA, lse=lg[b, h],
+                                               tol=TOL, rows=range(nv))
+                I, amb = I[:nv, :nv], amb[:nv, :nv]
+                listed = ~np.isnan(I)
+                got = after[b, h]
+                diff = np.abs(got - np.nan_to_num(I)) * np.outer(sizes, sizes)
+                assert (diff[listed] <= amb[listed] + 1e-6).all(), (b, h, float(diff[listed].max()))
+                if before is not None:
+                    assert (got[~listed] == before[b, h][~listed]).all()
+
+    full = [[[list(range(nt))] * nt for _ in range(H)] for _ in range(B)]
+    fidx, fcnt = _lists_tensors(cfg, full)
+    before = None
+    for t in (1, 2):
+        lse = attention(fidx, fcnt)
+        M.mod_update_stats(st.handle, qd, kd, lse, fidx, fcnt, t)
+        torch.cuda.synchronize()
+        after = M.mod_stats_get_block_mass(st.handle, B, H, nv)
+        check_counts(lse, full, before, after)
+        before = after
+        P.update_from_statistic(after.copy(), t)
+    idx = torch.empty((B, H, nt, nt), dtype=torch.int32, device="cuda")
+    cnt = torch.empty((B, H, nt), dtype=torch.int32, device="cuda")
+    budget = ("topk", 0.4)
+    for t in (3, 4, 5):
+        M.mod_predict_block_mask(st.handle, None, None, t, M.make_budget("topk", density=0.4), idx, cnt)
+        torch.cuda.synchronize()
+        sel = P.predict(None, None, t, O.Budget("topk", density=0.4))
+        rows = gpu_lists(idx, cnt)
+        po = P.prediction(t)
+        for b in range(B):
+            for h in range(H):
+                _check_text_head(P, rows[b][h], sel[b][h], *po[b][h], bool(P.gates[b, h]), budget)
+        if t == 4:
+            lse = attention(idx, cnt)
+            M.mod_update_stats(st.handle, qd, kd, lse, idx, cnt, t)
+            torch.cuda.synchronize()
+            after = M.mod_stats_get_block_mass(st.handle, B, H, nv)
+            check_counts(lse, rows, before, after)
+            listed = np.zeros((B, H, nv, nv), bool)
+            for b in range(B):
+                for h in range(H):
+                    for i in range(nv):
+                        js = [j for j in rows[b][h][i] if j < nv]
+                        listed[b, h, i, js] = True
+            P.update_from_statistic(np.where(listed, after, np.nan), t)
+            before = after
+    st.close()
+
+
+def test_text_shape_errors_on_device():
+    cfg = CONFIGS["tiny+40"]
+    with pytest.raises(M.ModError) as e:    # video part not whole frames
+        M.Stats(M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens, cfg.text_tokens + 1),
+                M.make_params())
+    assert e.value.status == M.MOD_ERR_UNSUPPORTED
+    st = M.Stats(_shape(cfg), M.make_params(warmup_m=1))
+    _, dev = _device(cfg)
+    M.mod_collect_stats(st.handle, dev[0], dev[1], 1)
+    nt, nv = st.n, st.n_video
+    idx = torch.empty((cfg.B, cfg.H, nt, nt), dtype=torch.int32, device="cuda")
+    cnt = torch.empty((cfg.B, cfg.H, nt), dtype=torch.int32, device="cuda")
+    with pytest.raises(M.ModError) as e:    # pattern K is counted over the video blocks
+        M.mod_predict_block_mask(st.handle, None, None, 2, M.make_budget("pattern", patterns=3 * nv), idx, cnt)
+    assert e.value.status == M.MOD_ERR_INVALID_ARG
+    M.mod_predict_block_mask(st.handle, None, None, 2, M.make_budget("pattern", patterns=3 * nv - 1), idx, cnt)
+    torch.cuda.synchronize()
+    assert (cnt.cpu().numpy() == nt).all()
+    st.close()
