@@ -54,8 +54,17 @@ WORKLOADS = {
     "wan-720p-d05": ("wan", "topk", 0.05),
     "hunyuan-720p-dense": ("hunyuan", "topk", 1.0),
     "hunyuan-720p-pattern": ("hunyuan", "pattern", 929),   # K = n patterns per head
+    # 256 text tokens after the video (token-type-aware masking): 931 blocks
+    "hunyuan-720p-text256": ("hunyuan+text256", "mass", 0.75),
     "small": ("small", "topk", 0.25),
 }
+
+
+def layer_config(W, name):
+    """A layer of the workload set; "<layer>+text<T>" appends T text tokens."""
+    base, _, text = name.partition("+text")
+    cfg = W.CONFIGS[base]
+    return W.with_text(cfg, int(text)) if text else cfg
 WARMUP_M = 5          # dense warm-up steps before the timed sparse steps
 
 
@@ -211,13 +220,13 @@ def cpu_baseline(cfg, host, rows_h0, mode, val, total_flops, sample_rows):
     k = W.bf16_bits_to_f64(host[1][:1, :1])
     v = W.bf16_bits_to_f64(host[2][0, 0])
     P = O.Predictor(1, 1, cfg.L, cfg.d, cfg.block, cfg.frame_tokens, warmup_m=WARMUP_M,
-                    delta_t=1)
+                    delta_t=1, text_tokens=cfg.text_tokens)
     P.collect(q, k, WARMUP_M - 1)
     P.collect(q, k, WARMUP_M)
     budget = O.Budget(mode, density=val if mode == "topk" else 1.0,
                       mass=val if mode == "mass" else 1.0,
                       patterns=int(val) if mode == "pattern" else 1)
-    n = P.n
+    n = P.n_total
     rows = [int(r) for r in np.linspace(0, n - 1, min(sample_rows, n)).round()]
     sizes = O.block_sizes(cfg.L, cfg.block)
     sflops = 4.0 * cfg.d * sum(int(sizes[i]) * int(sizes[np.asarray(rows_h0[i])].sum())
@@ -458,7 +467,7 @@ def main():
     import workloads as W
 
     cfg_name, mode, val = WORKLOADS[args.workload]
-    cfg = W.CONFIGS[cfg_name]
+    cfg = layer_config(W, cfg_name)
     t0 = time.perf_counter()
     host = W.generate(cfg)
     t_gen = time.perf_counter() - t0
@@ -470,7 +479,7 @@ def main():
         return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(dev)
 
     qd, kd, vd = (to_dev(x) for x in host)
-    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens, cfg.text_tokens)
     stats = M.Stats(shape, M.make_params(warmup_m=WARMUP_M, delta_t=1, tau_e=0.0, anchor_rule=0))
     n = stats.n
     budget = (M.make_budget(mode, density=val) if mode == "topk" else
@@ -537,7 +546,8 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"{args.workload} layer: B={cfg.B} H={cfg.H} L={cfg.L} d={cfg.d} "
-                        f"block={cfg.block} ({cfg.frames} frames x {cfg.hs}x{cfg.ws})",
+                        f"block={cfg.block} ({cfg.frames} frames x {cfg.hs}x{cfg.ws}"
+                        + (f" + {cfg.text_tokens} text tokens)" if cfg.text_tokens else ")"),
             "budget": f"{mode} {val}",
             "kept_density": round(density, 4),
             "kept_tflop": round(flops / 1e12, 3),
