@@ -196,7 +196,11 @@ mod_status mod_predict_block_mask(mod_stats* stats, const void* q, const void* k
                                   const mod_budget* budget, int32_t* kv_idx, int32_t* kv_cnt,
                                   void* stream);
 
-/* Device workspace the attention call needs (bytes; 0 means none). */
+/* Device workspace the attention call needs, in bytes (about
+ * 4 * B * H * (n/2 + 11); 0 for an invalid shape).  It holds the call's work
+ * plan: the (head, pair of query blocks) items ordered and spread over the
+ * chip by their list lengths.  Owned by the caller, rewritten by every call;
+ * two calls in flight at once need two workspaces. */
 size_t mod_attn_workspace_bytes(const mod_shape* shape);
 
 /* Block-sparse attention forward (Eq. 1 with the block mask of the lists):
@@ -208,8 +212,9 @@ size_t mod_attn_workspace_bytes(const mod_shape* shape);
  * kv_cnt = 0 gives O = 0 and lse = -inf.  scale = 0 means 1/sqrt(d).
  * q, k, v, o: [B,H,L,d] bf16 device; lse: [B,H,L] fp32 device or NULL.
  * bf16 MFMA products, fp32 softmax and accumulation.  `frame_tokens` and
- * `text_tokens` of the shape are not used.  workspace may be NULL when mod_attn_workspace_bytes
- * returns 0. */
+ * `text_tokens` of the shape are not used.  workspace: device memory of at
+ * least mod_attn_workspace_bytes(shape) bytes (ws_bytes), 16-byte aligned,
+ * else MOD_ERR_INVALID_ARG. */
 mod_status mod_block_sparse_attn_fwd(const mod_shape* shape, const void* q, const void* k,
                                      const void* v, const int32_t* kv_idx,
                                      const int32_t* kv_cnt, float scale, void* o, float* lse,

@@ -197,6 +197,12 @@ def mod_attn_workspace_bytes(shape: mod_shape) -> int:
 
 def mod_block_sparse_attn_fwd(shape: mod_shape, q, k, v, kv_idx, kv_cnt, scale: float, o,
                               lse=None, workspace=None, ws_bytes: int = 0, stream=None) -> None:
+    """workspace=None: a device buffer of mod_attn_workspace_bytes(shape)
+    bytes is allocated for the call (pass one to keep allocations out of a
+    loop)."""
+    if workspace is None and hasattr(q, "device"):
+        ws_bytes = mod_attn_workspace_bytes(shape)
+        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=q.device)
     _check(_lib.mod_block_sparse_attn_fwd(
         ctypes.byref(shape), _ptr(q, "q", "torch.bfloat16"), _ptr(k, "k", "torch.bfloat16"),
         _ptr(v, "v", "torch.bfloat16"), _ptr(kv_idx, "kv_idx", "torch.int32"),

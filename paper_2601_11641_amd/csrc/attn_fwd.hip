@@ -26,6 +26,7 @@
 // two buffers each: group 0 copies K, group 1 copies V, one tile ahead.
 #include "moddit_internal.h"
 
+#include <algorithm>
 #include <type_traits>
 
 namespace moddit {
@@ -146,12 +147,190 @@ struct TileCopy {
     }
 };
 
+// ---------------------------------------------------------------------------
+// Work plan.  The per-pair work (about the two rows' list lengths) varies
+// along the sequence and across heads, so a fixed pair -> XCD map leaves
+// some XCDs idle at the end.  Three small kernels write a plan into the
+// workspace before every attention launch:
+//   split  per head, the cost 4 + cnt(2p) + cnt(2p+1) of every pair p and
+//          eight contiguous pair ranges of about equal cost (pair p goes to
+//          range floor(8 * midpoint(p) / total)), one per XCD: neighbouring
+//          rows share K/V blocks, so an XCD's L2 serves its range;
+//   order  heads by decreasing total cost (ties by index; natural order
+//          above kPlanMaxHeads heads);
+//   lists  per XCD, its ranges of all heads in that order, as a list of
+//          items bh * npairs + p, plus its length, start and a zeroed
+//          fetch counter.
+// The attention work-groups are persistent (one per CU): a work-group
+// fetches the next item of its XCD's list with an atomic counter and, once
+// that list is drained, of the other XCDs' lists, until all are drained.
+// ---------------------------------------------------------------------------
+constexpr int kPlanThreads = 256;
+constexpr int kPlanMaxHeads = 4096;
+constexpr int kPlanHdr = 32;          // ints: ctr[8], len[8], start[8], pad
+
+struct Plan {
+    int* ctr;       // [8] fetch counters
+    int* len;       // [8] items per XCD list
+    int* start;     // [8] first item of each XCD list in `items`
+    int* tot;       // [BH] total cost per head
+    int* order;     // [BH] heads by decreasing cost
+    int* bounds;    // [BH][9] pair ranges per XCD
+    int* items;     // [BH * npairs]
+    __host__ __device__ Plan(void* ws, int BH) {
+        int* w = static_cast<int*>(ws);
+        ctr = w;
+        len = w + 8;
+        start = w + 16;
+        tot = w + kPlanHdr;
+        order = tot + BH;
+        bounds = order + BH;
+        items = bounds + 9 * BH;
+    }
+};
+
+__device__ __forceinline__ int clamp_count(const int32_t* kv_cnt, size_t row, int n) {
+    return min(max(kv_cnt[row], 0), n);
+}
+
+__global__ __launch_bounds__(kPlanThreads) void plan_split_kernel(const int32_t* __restrict__ kv_cnt,
+                                                                  void* ws, int BH, int n) {
+    __shared__ int scan[kPlanThreads];
+    __shared__ int below[kXcds];
+    const Plan pl(ws, BH);
+    const int bh = blockIdx.x, t = threadIdx.x;
+    const int npairs = (n + 1) / 2;
+    const int per = (npairs + kPlanThreads - 1) / kPlanThreads;   // pairs per thread, contiguous
+    auto cost = [&](int p) {
+        const size_t r0 = (size_t)bh * n + 2 * p;
+        return 4 + clamp_count(kv_cnt, r0, n) + (2 * p + 1 < n ? clamp_count(kv_cnt, r0 + 1, n) : 0);
+    };
+    int mine = 0;
+    for (int e = 0; e < per; ++e) {
+        const int p = t * per + e;
+        if (p < npairs) mine += cost(p);
+    }
+    scan[t] = mine;
+    if (t < kXcds) below[t] = 0;
+    __syncthreads();
+    for (int off = 1; off < kPlanThreads; off <<= 1) {   // inclusive scan
+        const int y = t >= off ? scan[t - off] : 0;
+        __syncthreads();
+        scan[t] += y;
+        __syncthreads();
+    }
+    const int total = scan[kPlanThreads - 1];
+    int run = scan[t] - mine;                               // cost before this thread's pairs
+    int cnt[kXcds] = {};
+    for (int e = 0; e < per; ++e) {
+        const int p = t * per + e;
+        if (p >= npairs) break;
+        const int c = cost(p);
+        // range of the pair's midpoint: floor(8 * (run + c/2) / total)
+        const int x = (int)min<long long>(kXcds - 1, ((long long)(2 * run + c) * kXcds) / (2LL * total));
+        for (int xx = x + 1; xx < kXcds; ++xx) ++cnt[xx];  // pairs below range xx
+        run += c;
+    }
+    for (int xx = 1; xx < kXcds; ++xx)
+        if (cnt[xx]) atomicAdd(&below[xx], cnt[xx]);
+    __syncthreads();
+    if (t == 0) {
+        int* b = pl.bounds + 9 * bh;
+        for (int xx = 0; xx < kXcds; ++xx) b[xx] = below[xx];
+        b[kXcds] = npairs;
+        pl.tot[bh] = total;
+    }
+}
+
+__global__ __launch_bounds__(kPlanThreads) void plan_order_kernel(void* ws, int BH) {
+    const Plan pl(ws, BH);
+    const int h = blockIdx.x * kPlanThreads + threadIdx.x;
+    if (h >= BH) return;
+    int rank = h;
+    if (BH <= kPlanMaxHeads) {
+        const int th = pl.tot[h];
+        rank = 0;
+        for (int o2 = 0; o2 < BH; ++o2) {
+            const int to = pl.tot[o2];
+            rank += (to > th || (to == th && o2 < h)) ? 1 : 0;
+        }
+    }
+    pl.order[rank] = h;
+}
+
+// one work-group per XCD list
+__global__ __launch_bounds__(kPlanThreads) void plan_lists_kernel(void* ws, int BH, int n) {
+    __shared__ int xtot[kXcds];
+    __shared__ int scan[kPlanThreads];
+    const Plan pl(ws, BH);
+    const int x = blockIdx.x, t = threadIdx.x;
+    const int npairs = (n + 1) / 2;
+    if (t < kXcds) xtot[t] = 0;
+    __syncthreads();
+    int part[kXcds] = {};
+    for (int h = t; h < BH; h += kPlanThreads) {
+        const int* b = pl.bounds + 9 * h;
+        for (int xx = 0; xx < kXcds; ++xx) part[xx] += b[xx + 1] - b[xx];
+    }
+    for (int xx = 0; xx < kXcds; ++xx)
+        if (part[xx]) atomicAdd(&xtot[xx], part[xx]);
+    __syncthreads();
+    int first = 0;
+    for (int xx = 0; xx < x; ++xx) first += xtot[xx];
+    // this XCD's range lengths in head order, blocked per thread, scanned
+    const int per = (BH + kPlanThreads - 1) / kPlanThreads;
+    int mine = 0;
+    for (int e = 0; e < per; ++e) {
+        const int s2 = t * per + e;
+        if (s2 < BH) {
+            const int* b = pl.bounds + 9 * pl.order[s2];
+            mine += b[x + 1] - b[x];
+        }
+    }
+    scan[t] = mine;
+    __syncthreads();
+    for (int off = 1; off < kPlanThreads; off <<= 1) {
+        const int y = t >= off ? scan[t - off] : 0;
+        __syncthreads();
+        scan[t] += y;
+        __syncthreads();
+    }
+    int pos = first + scan[t] - mine;
+    for (int e = 0; e < per; ++e) {
+        const int s2 = t * per + e;
+        if (s2 >= BH) break;
+        const int h = pl.order[s2];
+        const int* b = pl.bounds + 9 * h;
+        for (int p = b[x]; p < b[x + 1]; ++p) pl.items[pos++] = h * npairs + p;
+    }
+    if (t == 0) {
+        pl.len[x] = xtot[x];
+        pl.start[x] = first;
+        pl.ctr[x] = 0;
+    }
+}
+
+// Next item for a work-group on XCD x: its own list first, then the others
+// (-1 once every list is drained).  Device-scope atomics: the counters are
+// shared by every XCD.
+__device__ __forceinline__ int fetch_item(const Plan& pl, int x) {
+#pragma unroll 1
+    for (int a = 0; a < kXcds; ++a) {
+        const int xx = (x + a) % kXcds;
+        const int len = pl.len[xx];
+        if (len == 0) continue;
+        const int k = atomicAdd(&pl.ctr[xx], 1);
+        if (k < len) return pl.items[pl.start[xx] + k];
+    }
+    return -1;
+}
+
 template <int D, int BS>
 __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, const int32_t* __restrict__ kv_idx,
     const int32_t* __restrict__ kv_cnt, float scale, uint16_t* __restrict__ o,
-    float* __restrict__ lse, int L, int n) {
+    float* __restrict__ lse, int L, int n, void* ws, int BH) {
     constexpr int QW = BS / 32;        // waves per group = 32-row query slices of a block
     constexpr int NT = BS * 4;         // threads: two groups of QW waves
     constexpr int KVW = BS / 2;        // kv rows per unit (half a tile)
@@ -171,18 +350,26 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     __shared__ uint32_t ulist[kMaxBlocks];     // union of the two lists: j | membership << 16
     __shared__ uint8_t umask[kMaxBlocks];
     __shared__ int wsum[NT / 64];
+    __shared__ int item_s;
 
-    // Work-group -> (head, pair of query blocks 2p, 2p+1): dispatch puts
-    // work-group b on XCD b % 8; all XCDs work on one head at a time (its K/V
-    // stays in the shared last-level cache) and each takes a contiguous run of
-    // pairs (neighbouring rows share K/V blocks, so the XCD's L2 serves them).
-    // Padding slots exit at once.
+    // Persistent work-group on XCD blockIdx % 8 (dispatch order): items
+    // (head, pair of query blocks 2p, 2p+1) come from the plan.  Every
+    // per-item value is derived inside the loop from copies of the thread
+    // index and the workspace pointer that the compiler cannot see through,
+    // so nothing is hoisted out of the loop to stay live in registers.
+    for (;;) {
+    int tid = threadIdx.x;
+    void* wsi = ws;
+    asm volatile("" : "+v"(tid));
+    asm volatile("" : "+s"(wsi));
+    if (tid == 0) item_s = fetch_item(Plan(wsi, BH), blockIdx.x % kXcds);
+    __syncthreads();
+    const int item = item_s;
+    __syncthreads();   // item_s is rewritten only after every wave has read it
+    if (item < 0) break;
     const int npairs = (n + 1) / 2;
-    const int chunk = (npairs + kXcds - 1) / kXcds;
-    const int xcd = blockIdx.x % kXcds, r = blockIdx.x / kXcds;
-    const int bh = r / chunk, pr = xcd * chunk + r % chunk;
-    if (pr >= npairs) return;
-    const int tid = threadIdx.x, lane = tid & 63;
+    const int bh = item / npairs, pr = item % npairs;
+    const int lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
     const int h = lane >> 5, l32 = lane & 31;
     const int qw = w % QW, g = w / QW;          // query slice, group
@@ -511,16 +698,34 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
         if (lse != nullptr && h == 0)
             lse[(size_t)bh * L + qrow] = l > 0.0f ? m * scale + logf(l) : -INFINITY;
     }
+    }   // next item
+}
+
+int persistent_groups() {
+    static int cus = 0;
+    if (cus == 0) {
+        int dev = 0, c = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && c > 0)
+            cus = c;
+        else
+            cus = 256;
+    }
+    return cus;
 }
 
 template <int D, int BS>
 hipError_t launch(const uint16_t* q, const uint16_t* k, const uint16_t* v, const int32_t* kv_idx,
                   const int32_t* kv_cnt, float scale, uint16_t* o, float* lse, int BH, int L, int n,
-                  hipStream_t s) {
-    const unsigned npairs = (unsigned)(n + 1) / 2;
-    const unsigned chunk = (npairs + kXcds - 1) / kXcds;
-    hipLaunchKernelGGL((attn_fwd_kernel<D, BS>), dim3((unsigned)BH * chunk * kXcds), dim3(BS * 4), 0, s,
-                       q, k, v, kv_idx, kv_cnt, scale, o, lse, L, n);
+                  void* ws, hipStream_t s) {
+    hipLaunchKernelGGL(plan_split_kernel, dim3((unsigned)BH), dim3(kPlanThreads), 0, s, kv_cnt, ws, BH, n);
+    hipLaunchKernelGGL(plan_order_kernel, dim3((unsigned)((BH + kPlanThreads - 1) / kPlanThreads)),
+                       dim3(kPlanThreads), 0, s, ws, BH);
+    hipLaunchKernelGGL(plan_lists_kernel, dim3(kXcds), dim3(kPlanThreads), 0, s, ws, BH, n);
+    const long items = (long)BH * ((n + 1) / 2);
+    const unsigned groups = (unsigned)std::min<long>(persistent_groups(), items);
+    hipLaunchKernelGGL((attn_fwd_kernel<D, BS>), dim3(groups), dim3(BS * 4), 0, s,
+                       q, k, v, kv_idx, kv_cnt, scale, o, lse, L, n, ws, BH);
     return hipGetLastError();
 }
 
@@ -634,14 +839,19 @@ hipError_t launch_count(const uint16_t* q, const uint16_t* k, const int32_t* kv_
 
 }  // namespace
 
+size_t attn_workspace_bytes(int BH, int n) {
+    const size_t ints = (size_t)kPlanHdr + (size_t)BH * (11 + (size_t)(n + 1) / 2);
+    return (ints * sizeof(int) + 255) / 256 * 256;
+}
+
 hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                            const int32_t* kv_idx, const int32_t* kv_cnt, float scale,
                            uint16_t* o, float* lse, int BH, int L, int d, int bs, int n,
-                           hipStream_t s) {
-    if (d == 128 && bs == 128) return launch<128, 128>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, s);
-    if (d == 128 && bs == 64) return launch<128, 64>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, s);
-    if (d == 64 && bs == 128) return launch<64, 128>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, s);
-    return launch<64, 64>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, s);
+                           void* ws, hipStream_t s) {
+    if (d == 128 && bs == 128) return launch<128, 128>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, ws, s);
+    if (d == 128 && bs == 64) return launch<128, 64>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, ws, s);
+    if (d == 64 && bs == 128) return launch<64, 128>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, ws, s);
+    return launch<64, 64>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, ws, s);
 }
 
 hipError_t launch_stat_count(const uint16_t* q, const uint16_t* k, const int32_t* kv_idx,

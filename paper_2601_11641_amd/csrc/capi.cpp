@@ -492,20 +492,24 @@ mod_status mod_predict_block_mask(mod_stats* s, const void* q, const void* k, in
 }
 
 size_t mod_attn_workspace_bytes(const mod_shape* shape) {
-    (void)shape;
-    return 0;
+    if (check_shape(shape, false) != MOD_OK) return 0;
+    return moddit::attn_workspace_bytes(shape->B * shape->H, ceil_div(shape->L, shape->block));
 }
 
 mod_status mod_block_sparse_attn_fwd(const mod_shape* shape, const void* q, const void* k,
                                      const void* v, const int32_t* kv_idx, const int32_t* kv_cnt,
                                      float scale, void* o, float* lse, void* workspace,
                                      size_t ws_bytes, void* stream) {
-    (void)workspace;
-    (void)ws_bytes;
     mod_status st = check_shape(shape, false);
     if (st != MOD_OK) return st;
     if (!q || !k || !v || !o || !kv_idx || !kv_cnt)
         return fail(MOD_ERR_INVALID_ARG, "q, k, v, o, kv_idx and kv_cnt must not be NULL");
+    const size_t need = moddit::attn_workspace_bytes(shape->B * shape->H, ceil_div(shape->L, shape->block));
+    if (!workspace || ws_bytes < need)
+        return fail(MOD_ERR_INVALID_ARG, "workspace of %zu bytes needed (got %zu%s)", need, ws_bytes,
+                    workspace ? "" : ", NULL");
+    if (reinterpret_cast<uintptr_t>(workspace) % 16 != 0)
+        return fail(MOD_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
     if (!(scale >= 0.0f) || !std::isfinite(scale))
         return fail(MOD_ERR_INVALID_ARG, "scale must be finite and >= 0");
     const float sc = scale == 0.0f ? (float)(1.0 / std::sqrt((double)shape->d)) : scale;
@@ -513,7 +517,7 @@ mod_status mod_block_sparse_attn_fwd(const mod_shape* shape, const void* q, cons
     hipError_t e = moddit::launch_attn_fwd(
         static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
         kv_idx, kv_cnt, sc, static_cast<uint16_t*>(o), lse, shape->B * shape->H, shape->L, shape->d,
-        shape->block, n, static_cast<hipStream_t>(stream));
+        shape->block, n, workspace, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "attention launch");
     return MOD_OK;
 }

@@ -53,11 +53,13 @@ hipError_t launch_select_patterns(const double* pred, const int32_t* gate, const
                                   const int* row_hi, int K, uint8_t* chosen, int32_t* kv_idx,
                                   int32_t* kv_cnt, int BH, int n, int ldn, int tb0, hipStream_t s);
 
-// a6: block-sparse attention forward.
+// a6: block-sparse attention forward.  ws: device workspace of
+// attn_workspace_bytes(BH, n) bytes (the work plan, rewritten every call).
+size_t attn_workspace_bytes(int BH, int n);
 hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                            const int32_t* kv_idx, const int32_t* kv_cnt, float scale,
                            uint16_t* o, float* lse, int BH, int L, int d, int bs, int n,
-                           hipStream_t s);
+                           void* ws, hipStream_t s);
 
 // Eq. 2 statistic of a computed attention map: stat[bh][i][j] = fraction of
 // the probabilities of listed block (i, j) that reach exp(log_eta), with the
