@@ -13,10 +13,11 @@
 //      and the product of the previous unit, O^T (d x q) += V^T . P^T, whose
 //      V^T operand comes from the row-major V tile through
 //      ds_read_b64_tr_b16 (transposing LDS reads);
-//   X  the softmax step: row max, lazy rescale (the running max only moves
-//      when a tile's max exceeds it by more than 2^8 in probability units),
-//      P = exp2(S * scale*log2e - m) in fp32, rounded to bf16 as the B
-//      operand of the next product without moving between lanes.
+//   X  the softmax step: P = exp2(S * scale*log2e - m) in fp32 with the
+//      running max m kept, accepted when no lane's probabilities of the unit
+//      sum past 2^8; otherwise (rarely) the unit's max is taken, m moves up
+//      to it and O, l are rescaled.  P is rounded to bf16 as the B operand of
+//      the next product without moving between lanes.
 // Waves of the two groups share every SIMD, and group 1 runs one phase behind
 // group 0 with a work-group barrier after every phase: on each SIMD one wave's
 // matrix products overlap the other wave's softmax.
@@ -39,7 +40,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kRescaleLog2 = 8.0f;   // lazy-rescale threshold (log2 units)
+constexpr float kSumLimit = 256.0f;    // fast-path bound on a lane's probability sum per unit
 constexpr int kXcds = 8;               // accelerator complex dies of an MI355X
 
 // max(x, x of lane l ^ 32): with x in both operands, v_permlane32_swap
@@ -451,7 +452,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     bf16x8 pb[2 * RT];   // P of the pending product: zero until a unit is computed
 #pragma unroll
     for (int c = 0; c < 2 * RT; ++c) pb[c] = bf16x8{};
-    float m = -INFINITY, l = 0.0f;
+    float m = -INFINITY, mb = 0.0f, l = 0.0f;   // running max, m * scale * log2(e), row sum
 
     const Copy copy(lane);
     const uint16_t* kg = k + base;
@@ -533,10 +534,38 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     };
 
     // X phase of a unit (kv rows half*KVW .. of a tile with kvalid valid
-    // rows): one online-softmax step, P rounded to bf16 in pb.  The copies
-    // cg (a full tile's source, or nullptr) into ct are spread over the
-    // exponentials; register fences keep each group of exponentials ahead of
-    // the next copy.
+    // rows): one online-softmax step, P rounded to bf16 in pb.
+    // Fast path: the running max m is kept and P = exp2(S*c2 - m*c2) is
+    // computed at once; it stands if no lane's probabilities of the unit sum
+    // to more than kSumLimit (so none exceeds it: P and the row sums stay well
+    // inside fp32 and bf16 range).  Otherwise (and while a row has seen no
+    // key yet) the slow path takes the unit's max, moves m up to it, rescales
+    // O and l, and computes P again.  The copies cg (a full tile's source,
+    // or nullptr) into ct are spread over the fast path's exponentials
+    // (register fences keep each group ahead of the next copy), or issued at
+    // once by the slow path when the fast path did not run.
+    auto exps = [&](auto copies_tag, const char* cgx, char* ct, float& ps0, float& ps1) __attribute__((always_inline)) {
+        constexpr bool copies = decltype(copies_tag)::value;
+        constexpr int NE = RT * 16;
+        static_assert(NE % IPW == 0, "copies must spread evenly over the exponentials");
+        ps0 = 0.0f;
+        ps1 = 0.0f;
+#pragma unroll
+        for (int qq = 0; qq < NE; ++qq) {
+            if (copies && qq % (NE / IPW) == 0) copy.issue_one(cgx, qq / (NE / IPW), ct, qw);
+            const int rt = qq / 16, c1 = (qq / 8) % 2, e = qq % 8;
+            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[rt][8 * c1 + e], c2, -mb));
+            pb[2 * rt + c1][e] = static_cast<__bf16>(p);
+            if (qq % 2 == 0)
+                ps0 += p;
+            else
+                ps1 += p;
+            if (qq % (NE / IPW) == NE / IPW - 1)
+                asm volatile("" : "+v"(pb[2 * rt + c1]), "+v"(ps0), "+v"(ps1));
+        }
+#pragma unroll
+        for (int c = 0; c < 2 * RT; ++c) asm volatile("" : "+v"(pb[c]));
+    };
     auto xphase = [&](int kvalid, auto half_tag, const char* cg, char* ct) __attribute__((always_inline)) {
         constexpr int half = decltype(half_tag)::value;
         if (kvalid < BS) {
@@ -550,56 +579,53 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
                     sacc[rt][ii] = (8 * (ii >> 2) + (ii & 3) >= lim) ? -INFINITY : sacc[rt][ii];
             }
         }
-        // tree of 3-input maxima (short dependency chains)
-        float t1[RT * 6];
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt) {
-#pragma unroll
-            for (int gq = 0; gq < 5; ++gq)
-                t1[6 * rt + gq] = fmaxf(sacc[rt][3 * gq], fmaxf(sacc[rt][3 * gq + 1], sacc[rt][3 * gq + 2]));
-            t1[6 * rt + 5] = sacc[rt][15];
-        }
-        float mx;
-        if constexpr (RT == 2) {
-            const float u0 = fmaxf(t1[0], fmaxf(t1[1], t1[2]));
-            const float u1 = fmaxf(t1[3], fmaxf(t1[4], t1[5]));
-            const float u2 = fmaxf(t1[6], fmaxf(t1[7], t1[8]));
-            const float u3 = fmaxf(t1[9], fmaxf(t1[10], t1[11]));
-            mx = fmaxf(fmaxf(u0, u1), fmaxf(u2, u3));
-        } else {
-            mx = fmaxf(fmaxf(t1[0], fmaxf(t1[1], t1[2])), fmaxf(t1[3], fmaxf(t1[4], t1[5])));
-        }
-        mx = max_across_halves(mx);
-        const bool need = (mx - m) * c2 > kRescaleLog2;
-        const float m_new = need ? mx : m;
-        const float alpha = need ? __builtin_amdgcn_exp2f((m - mx) * c2) : 1.0f;
-        const float mb = m_new == -INFINITY ? 0.0f : m_new * c2;
-        if (__any(need)) {
-            asm volatile("" ::: "memory");
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
-        }
-        constexpr int NE = RT * 16;
-        static_assert(NE % IPW == 0, "copies must spread evenly over the exponentials");
-        float ps0 = 0.0f, ps1 = 0.0f;
-#pragma unroll
-        for (int qq = 0; qq < NE; ++qq) {
-            if (cg != nullptr && qq % (NE / IPW) == 0) copy.issue_one(cg, qq / (NE / IPW), ct, qw);
-            const int rt = qq / 16, c1 = (qq / 8) % 2, e = qq % 8;
-            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[rt][8 * c1 + e], c2, -mb));
-            pb[2 * rt + c1][e] = static_cast<__bf16>(p);
-            if (qq % 2 == 0)
-                ps0 += p;
+        float ps0, ps1;
+        bool fast = __all(m > -INFINITY);
+        if (fast) {
+            if (cg != nullptr)
+                exps(yes{}, cg, ct, ps0, ps1);
             else
-                ps1 += p;
-            if (qq % (NE / IPW) == NE / IPW - 1)
-                asm volatile("" : "+v"(pb[2 * rt + c1]), "+v"(ps0), "+v"(ps1));
-        }
-        l = l * alpha + (ps0 + ps1);
-        m = m_new;
+                exps(std::false_type{}, nullptr, ct, ps0, ps1);
+            fast = !__any(!(ps0 + ps1 <= kSumLimit));
+        } else if (cg != nullptr) {
 #pragma unroll
-        for (int c = 0; c < 2 * RT; ++c) asm volatile("" : "+v"(pb[c]));
-        asm volatile("" : "+v"(l), "+v"(m));
+            for (int ii = 0; ii < IPW; ++ii) copy.issue_one(cg, ii, ct, qw);
+        }
+        if (!fast) {
+            asm volatile("" ::: "memory");
+            // tree of 3-input maxima (short dependency chains)
+            float t1[RT * 6];
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+                for (int gq = 0; gq < 5; ++gq)
+                    t1[6 * rt + gq] = fmaxf(sacc[rt][3 * gq], fmaxf(sacc[rt][3 * gq + 1], sacc[rt][3 * gq + 2]));
+                t1[6 * rt + 5] = sacc[rt][15];
+            }
+            float mx;
+            if constexpr (RT == 2) {
+                const float u0 = fmaxf(t1[0], fmaxf(t1[1], t1[2]));
+                const float u1 = fmaxf(t1[3], fmaxf(t1[4], t1[5]));
+                const float u2 = fmaxf(t1[6], fmaxf(t1[7], t1[8]));
+                const float u3 = fmaxf(t1[9], fmaxf(t1[10], t1[11]));
+                mx = fmaxf(fmaxf(u0, u1), fmaxf(u2, u3));
+            } else {
+                mx = fmaxf(fmaxf(t1[0], fmaxf(t1[1], t1[2])), fmaxf(t1[3], fmaxf(t1[4], t1[5])));
+            }
+            mx = max_across_halves(mx);
+            const float m_new = fmaxf(m, mx);
+            const float alpha = m_new == m ? 1.0f : __builtin_amdgcn_exp2f((m - m_new) * c2);
+            if (__any(alpha != 1.0f)) {
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
+                l *= alpha;
+            }
+            m = m_new;
+            mb = m_new == -INFINITY ? 0.0f : m_new * c2;
+            exps(std::false_type{}, nullptr, ct, ps0, ps1);
+        }
+        l += ps0 + ps1;
+        asm volatile("" : "+v"(l), "+v"(m), "+v"(mb));
     };
 
     // ---- schedule ----
