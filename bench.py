@@ -88,6 +88,9 @@ def parse():
                     help="50-step denoising schedule on the Hunyuan 720p shape (5 dense warm-up "
                          "steps, 45 predicted sparse steps) for re-anchor intervals 10 and 1; one "
                          "JSON line per interval")
+    ap.add_argument("--trace-summary", nargs=2, metavar=("STATS_CSV", "BENCH_LOG"),
+                    help="format a rocprofv3 --kernel-trace --stats CSV of a bench run (and the JSON "
+                         "line that run printed) into profiles/hunyuan720p_step_kernel_stats.md and exit")
     ap.add_argument("--counter-summary", metavar="PMC_DIR",
                     help="summarise rocprofv3 counter passes A..F found under PMC_DIR/<pass>/ "
                          "into profiles/ and exit")
@@ -98,6 +101,52 @@ def source_digest() -> str:
     import hashlib
     with open(ATTN_SOURCE, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+TRACE_SUMMARY = os.path.join(ROOT, "profiles", "hunyuan720p_step_kernel_stats.md")
+TRACE_COMMAND = ("rocprofv3 --kernel-trace --stats -d gpurun_out/prof -o bench --output-format csv "
+                 "-- python3 bench.py --steps 5 --warmup 2 --no-cpu-baseline")
+
+
+def summarize_trace(stats_csv: str, bench_log: str):
+    """Per-kernel time table of one profiled bench run (rocprofv3 kernel
+    statistics), with the attention kernel's average checked against the
+    event timing that bench.py printed for the same launches."""
+    import csv
+    import re
+    with open(stats_csv) as f:
+        rows = list(csv.DictReader(f))
+    line = None
+    with open(bench_log) as f:
+        for t in f:
+            if t.startswith("{"):
+                line = json.loads(t)
+    cfg = line["config"]
+    total = sum(float(r["TotalDurationNs"]) for r in rows if "moddit" in r["Name"])
+    out = ["# Kernel time summary: hunyuan-720p layer step", "",
+           "Command (repo root, MI355X):", "", "    " + TRACE_COMMAND, "",
+           f"Workload: {cfg['workload']}, {cfg['budget']} budget, kept density "
+           f"{cfg['kept_density']}, kept work {cfg['kept_tflop']} TFLOP per step.",
+           f"bench.py under the profiler reported attn_ms {cfg['attn_ms']} (HIP events on the launch "
+           f"stream), predict_ms {cfg['predict_ms']}.", "",
+           "| kernel | calls | avg us | share |", "|---|---|---|---|"]
+    attn_avg = None
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        if "moddit" not in r["Name"]:
+            continue
+        name = re.sub(r"^void ", "", r["Name"])
+        name = re.sub(r"moddit::\(anonymous namespace\)::", "", name)
+        name = re.sub(r"\(.*$", "", name)
+        avg = float(r["AverageNs"]) / 1e3
+        if name.startswith("attn_fwd_kernel"):
+            attn_avg = avg
+        out.append(f"| {name} | {r['Calls']} | {avg:.1f} | {100 * float(r['TotalDurationNs']) / total:.2f}% |")
+    out += ["", "Torch helper kernels of the kept-flop accounting (after the timed region) are omitted.",
+            f"attn_fwd_kernel average {attn_avg:.1f} us against bench.py's event timing of the same "
+            f"launches ({cfg['attn_ms']} ms)."]
+    with open(TRACE_SUMMARY, "w") as f:
+        f.write("\n".join(out) + "\n")
+    print("\n".join(out))
 
 
 def summarize_counters(pmc_dir: str):
@@ -449,6 +498,9 @@ def main():
 
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.trace_summary:
+        summarize_trace(*args.trace_summary)
         return
     if args.counter_summary:
         summarize_counters(args.counter_summary)

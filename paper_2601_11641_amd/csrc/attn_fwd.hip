@@ -541,9 +541,9 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     // inside fp32 and bf16 range).  Otherwise (and while a row has seen no
     // key yet) the slow path takes the unit's max, moves m up to it, rescales
     // O and l, and computes P again.  The copies cg (a full tile's source,
-    // or nullptr) into ct are spread over the fast path's exponentials
-    // (register fences keep each group ahead of the next copy), or issued at
-    // once by the slow path when the fast path did not run.
+    // or nullptr) into ct are interleaved with the fast path's exponentials
+    // (the compiler schedules them), or issued at once by the slow path when
+    // the fast path did not run.
     auto exps = [&](auto copies_tag, const char* cgx, char* ct, float& ps0, float& ps1) __attribute__((always_inline)) {
         constexpr bool copies = decltype(copies_tag)::value;
         constexpr int NE = RT * 16;
@@ -560,8 +560,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
                 ps0 += p;
             else
                 ps1 += p;
-            if (qq % (NE / IPW) == NE / IPW - 1)
-                asm volatile("" : "+v"(pb[2 * rt + c1]), "+v"(ps0), "+v"(ps1));
+
         }
 #pragma unroll
         for (int c = 0; c < 2 * RT; ++c) asm volatile("" : "+v"(pb[c]));
