@@ -155,7 +155,7 @@ mod_status mod_collect_stats(mod_stats* stats, const void* q, const void* k, int
  *   I(i, j) = 1 - S(i, j) = fraction of the probabilities
  *             exp(scale * Q_p.K_q - lse_p), p in i, q in j, that reach eta
  * (S of Eq. 2 over the block's valid entries; decided in fp32 as
- * scale * s >= lse_p + log(eta), s the fp32 product of the bf16 inputs)
+ * s >= (lse_p + log(eta)) / scale, s the fp32 product of the bf16 inputs)
  * replaces the stored value; unlisted blocks keep their previous value
  * (Eq. 5 at block level).  The MOD model is then fitted to the whole stored
  * map and (step, X) becomes the newest anchor.  The first update should

@@ -326,66 +326,21 @@ __device__ __forceinline__ int fetch_item(const Plan& pl, int x) {
     return -1;
 }
 
-template <int D, int BS>
-__global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
-    const uint16_t* __restrict__ v, const int32_t* __restrict__ kv_idx,
-    const int32_t* __restrict__ kv_cnt, float scale, uint16_t* __restrict__ o,
-    float* __restrict__ lse, int L, int n, void* ws, int BH) {
-    constexpr int QW = BS / 32;        // waves per group = 32-row query slices of a block
-    constexpr int NT = BS * 4;         // threads: two groups of QW waves
-    constexpr int KVW = BS / 2;        // kv rows per unit (half a tile)
-    constexpr int RT = KVW / 32;       // 32-row kv sub-tiles per unit
-    constexpr int DT = D / 32;         // 32-row d tiles of O^T
-    constexpr int KK = D / 16;         // 16-deep d chunks of S^T
-    constexpr int TILE = BS * D * 2;   // bytes per K or V tile
-    constexpr int ROWB = 2 * D;
-    constexpr int HALF = KVW * ROWB;   // bytes per half tile
+// Union of the kv lists of rows row0 and row0 + 1 (the second only if has1)
+// of the [rows, n] lists, compacted in ascending j into ulist as
+// j | membership << 16 (bit 0: row0, bit 1: row0 + 1).  Counts are clamped to
+// [0, n] (a row never reads past its n entries), entries outside [0, n) are
+// ignored and a repeated entry counts once.  Every thread of the NT-thread
+// work-group calls it; ulist is complete after the caller's next barrier.
+template <int NT>
+__device__ __forceinline__ int union_of_rows(const int32_t* __restrict__ kv_idx,
+                                             const int32_t* __restrict__ kv_cnt, size_t row0, bool has1,
+                                             int n, uint8_t* umask, uint32_t* ulist, int* wsum, int tid,
+                                             int lane, int w) {
     constexpr int JPT = kMaxBlocks / NT;
-    using Copy = TileCopy<D, BS, QW>;
-    constexpr int IPW = Copy::IPW;
-    __shared__ __align__(1024) char kb0[TILE];
-    __shared__ __align__(1024) char kb1[TILE];
-    __shared__ __align__(1024) char vb0[TILE];
-    __shared__ __align__(1024) char vb1[TILE];
-    __shared__ uint32_t ulist[kMaxBlocks];     // union of the two lists: j | membership << 16
-    __shared__ uint8_t umask[kMaxBlocks];
-    __shared__ int wsum[NT / 64];
-    __shared__ int item_s;
-
-    // Persistent work-group on XCD blockIdx % 8 (dispatch order): items
-    // (head, pair of query blocks 2p, 2p+1) come from the plan.  Every
-    // per-item value is derived inside the loop from copies of the thread
-    // index and the workspace pointer that the compiler cannot see through,
-    // so nothing is hoisted out of the loop to stay live in registers.
-    for (;;) {
-    int tid = threadIdx.x;
-    void* wsi = ws;
-    asm volatile("" : "+v"(tid));
-    asm volatile("" : "+s"(wsi));
-    if (tid == 0) item_s = fetch_item(Plan(wsi, BH), blockIdx.x % kXcds);
-    __syncthreads();
-    const int item = item_s;
-    __syncthreads();   // item_s is rewritten only after every wave has read it
-    if (item < 0) break;
-    const int npairs = (n + 1) / 2;
-    const int bh = item / npairs, pr = item % npairs;
-    const int lane = tid & 63;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
-    const int h = lane >> 5, l32 = lane & 31;
-    const int qw = w % QW, g = w / QW;          // query slice, group
-    const int i = 2 * pr + g;                   // this group's query block (n: none)
-    const size_t base = (size_t)bh * L * D;
-    const float c2 = scale * kLog2e;
-    const int qrow = i * BS + 32 * qw + l32;
-
-    // ---- union of the kv lists of blocks 2p and 2p+1, ascending j ----
-    // (entries outside [0, n) are ignored; a repeated entry counts once)
-    const int i0 = 2 * pr, i1 = 2 * pr + 1;
-    // counts are clamped to [0, n]: a row never reads past its n entries
-    const int cnt0 = min(max(kv_cnt[bh * n + i0], 0), n);
-    const int cnt1 = i1 < n ? min(max(kv_cnt[bh * n + i1], 0), n) : 0;
-    const int32_t* list0 = kv_idx + (size_t)(bh * n + i0) * n;
+    const int cnt0 = min(max(kv_cnt[row0], 0), n);
+    const int cnt1 = has1 ? min(max(kv_cnt[row0 + 1], 0), n) : 0;
+    const int32_t* list0 = kv_idx + row0 * n;
     const int32_t* list1 = list0 + n;
     for (int j = tid; j < n; j += NT) umask[j] = 0;
     __syncthreads();
@@ -425,6 +380,64 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
         const int j = tid * JPT + e;
         if (j < n && umask[j] != 0) ulist[pos++] = (uint32_t)j | ((uint32_t)umask[j] << 16);
     }
+    return ucnt;
+}
+
+template <int D, int BS>
+__global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+    const uint16_t* __restrict__ v, const int32_t* __restrict__ kv_idx,
+    const int32_t* __restrict__ kv_cnt, float scale, uint16_t* __restrict__ o,
+    float* __restrict__ lse, int L, int n, void* ws, int BH) {
+    constexpr int QW = BS / 32;        // waves per group = 32-row query slices of a block
+    constexpr int NT = BS * 4;         // threads: two groups of QW waves
+    constexpr int KVW = BS / 2;        // kv rows per unit (half a tile)
+    constexpr int RT = KVW / 32;       // 32-row kv sub-tiles per unit
+    constexpr int DT = D / 32;         // 32-row d tiles of O^T
+    constexpr int KK = D / 16;         // 16-deep d chunks of S^T
+    constexpr int TILE = BS * D * 2;   // bytes per K or V tile
+    constexpr int ROWB = 2 * D;
+    constexpr int HALF = KVW * ROWB;   // bytes per half tile
+    using Copy = TileCopy<D, BS, QW>;
+    constexpr int IPW = Copy::IPW;
+    __shared__ __align__(1024) char kb0[TILE];
+    __shared__ __align__(1024) char kb1[TILE];
+    __shared__ __align__(1024) char vb0[TILE];
+    __shared__ __align__(1024) char vb1[TILE];
+    __shared__ uint32_t ulist[kMaxBlocks];     // union of the two lists: j | membership << 16
+    __shared__ uint8_t umask[kMaxBlocks];
+    __shared__ int wsum[NT / 64];
+    __shared__ int item_s;
+
+    // Persistent work-group on XCD blockIdx % 8 (dispatch order): items
+    // (head, pair of query blocks 2p, 2p+1) come from the plan.  Every
+    // per-item value is derived inside the loop from copies of the thread
+    // index and the workspace pointer that the compiler cannot see through,
+    // so nothing is hoisted out of the loop to stay live in registers.
+    for (;;) {
+    int tid = threadIdx.x;
+    void* wsi = ws;
+    asm volatile("" : "+v"(tid));
+    asm volatile("" : "+s"(wsi));
+    if (tid == 0) item_s = fetch_item(Plan(wsi, BH), blockIdx.x % kXcds);
+    __syncthreads();
+    const int item = item_s;
+    __syncthreads();   // item_s is rewritten only after every wave has read it
+    if (item < 0) break;
+    const int npairs = (n + 1) / 2;
+    const int bh = item / npairs, pr = item % npairs;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
+    const int h = lane >> 5, l32 = lane & 31;
+    const int qw = w % QW, g = w / QW;          // query slice, group
+    const int i = 2 * pr + g;                   // this group's query block (n: none)
+    const size_t base = (size_t)bh * L * D;
+    const float c2 = scale * kLog2e;
+    const int qrow = i * BS + 32 * qw + l32;
+
+    // ---- union of the kv lists of blocks 2p and 2p+1, ascending j ----
+    const size_t row0 = (size_t)bh * n + 2 * pr;
+    const int ucnt = union_of_rows<NT>(kv_idx, kv_cnt, row0, 2 * pr + 1 < n, n, umask, ulist, wsum, tid, lane, w);
     // The first product (before any unit has been computed) multiplies a
     // zero P with the second half of the "previous" V buffer: that half
     // holds zeros rather than whatever the LDS held before.
@@ -760,94 +773,115 @@ hipError_t launch(const uint16_t* q, const uint16_t* k, const uint16_t* v, const
 // block (i, j), the fraction of the probabilities exp(scale q_p.k_q - LSE_p)
 // that reach eta, LSE_p being the row LSE the attention forward returned
 // over the same lists (the masked map; all blocks at a dense step).  The
-// decision is taken in fp32: scale * s >= LSE_p + log(eta), s the fp32 MFMA
-// product.  One work-group per (head, query block), BS/32 waves of 32 query
-// rows; the K tiles of the row's list are copied into LDS one tile ahead.
-// The result is written into stat[bh][i][j] (fp64); blocks not listed keep
-// their previous value (the reconstruction of Eq. 5).
+// decision is taken in fp32 as s >= (LSE_p + log(eta)) / scale, s the fp32
+// MFMA product.  Like the attention, one work-group per (head, pair of query
+// blocks 2p, 2p+1) walks the union of the two lists with two groups of BS/32
+// waves (32 query rows each), so every K tile copied into LDS serves both
+// blocks; K tiles are double-buffered and copied by all waves one tile ahead.
+// A lane counts its own products, the wave sums over lanes, and the
+// group's count of a tile is written into stat[bh][i][j] (fp64) after the
+// tile's barrier; blocks not listed keep their previous value (the
+// reconstruction of Eq. 5).
 // With a text segment after the video the lists cover all n blocks of the
 // sequence while the statistic covers the first nv (video) blocks: rows
 // i < nv are counted and only entries j < nv are stored (stat [BH, nv, nv]).
 // ---------------------------------------------------------------------------
 template <int D, int BS>
-__global__ __launch_bounds__(BS * 2, 1) void stat_count_kernel(
+__global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const int32_t* __restrict__ kv_idx, const int32_t* __restrict__ kv_cnt,
     const float* __restrict__ lse, float scale, float log_eta, double* __restrict__ stat, int L, int n,
     int nv) {
-    constexpr int QW = BS / 32;        // waves, 32 query rows each
+    constexpr int QW = BS / 32;        // waves per group, 32 query rows each
+    constexpr int NT = BS * 4;         // two groups
     constexpr int RT = BS / 32;        // 32-row kv sub-tiles per tile
     constexpr int KK = D / 16;
     constexpr int TILE = BS * D * 2;
     constexpr int ROWB = 2 * D;
-    using Copy = TileCopy<D, BS, QW>;
-    __shared__ __align__(1024) char kb0[TILE];
-    __shared__ __align__(1024) char kb1[TILE];
-    __shared__ int part[2][QW];
+    using Copy = TileCopy<D, BS, 2 * QW>;
+    __shared__ __align__(1024) char kbuf[2][TILE];   // K tiles, double-buffered
+    __shared__ uint32_t ulist[kMaxBlocks];
+    __shared__ uint8_t umask[kMaxBlocks];
+    __shared__ int wsum[NT / 64];
+    __shared__ int part[2][2][QW];
 
-    const int bh = blockIdx.x / nv, i = blockIdx.x % nv;
-    const size_t item = (size_t)bh * n + i;    // row of the lists
+    const int npv = (nv + 1) / 2;      // pairs of video rows
+    const int bh = blockIdx.x / npv, pr = blockIdx.x % npv;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int h = lane >> 5, l32 = lane & 31;
+    const int qw = w % QW, g = w / QW;
+    const int i = 2 * pr + g;          // this group's query block (nv: none)
     const size_t base = (size_t)bh * L * D;
-    const int qrow = i * BS + 32 * w + l32;
+    const int qrow = i * BS + 32 * qw + l32;
+    const bool row_ok = i < nv && qrow < L;
     const int rows_i = min(BS, L - i * BS);
+
+    const size_t row0 = (size_t)bh * n + 2 * pr;
+    const int ucnt = union_of_rows<NT>(kv_idx, kv_cnt, row0, 2 * pr + 1 < nv, n, umask, ulist, wsum, tid,
+                                       lane, w);
 
     bf16x8 qreg[KK];
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
         uint4 val = make_uint4(0, 0, 0, 0);
-        if (qrow < L)
-            val = *reinterpret_cast<const uint4*>(q + base + (size_t)qrow * D + 16 * kk + 8 * h);
+        if (row_ok) val = *reinterpret_cast<const uint4*>(q + base + (size_t)qrow * D + 16 * kk + 8 * h);
         qreg[kk] = __builtin_bit_cast(bf16x8, val);
     }
-    // a row past the end of the sequence never counts
-    const float thr = qrow < L ? lse[(size_t)bh * L + qrow] + log_eta : INFINITY;
+    // a row past the end of the sequence (or of the video rows) never counts
+    const float thr = row_ok ? (lse[(size_t)bh * L + qrow] + log_eta) / scale : INFINITY;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) asm volatile("" : "+v"(qreg[kk]));
+    __syncthreads();   // publishes the union list
 
-    const int cnt = min(max(kv_cnt[item], 0), n);   // never past the row's n entries
-    const int32_t* list = kv_idx + (size_t)item * n;
     const Copy copy(lane);
     const uint16_t* kg = k + base;
     const int ka = l32 * ROWB + ((h ^ swz<D>(l32)) << 4);
-    // entries outside [0, n) are skipped (their copy reads block 0)
-    auto block_of = [&](int t) { const int j = list[t]; return (unsigned)j < (unsigned)n ? j : -1; };
-    if (cnt > 0) copy.issue_all(kg, max(block_of(0), 0), L, kb0, w, lane);
+    // tile t+1 is copied while tile t is counted (its buffer was last read
+    // while counting tile t-1)
+    if (ucnt > 0) copy.issue_all(kg, (int)(ulist[0] & 0xFFFF), L, kbuf[0], w, lane);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    for (int t = 0; t < cnt; ++t) {
-        const char* cur = (t & 1) ? kb1 : kb0;
-        char* nxt = (t & 1) ? kb0 : kb1;
-        if (t + 1 < cnt) copy.issue_all(kg, max(block_of(t + 1), 0), L, nxt, w, lane);
-        const int j = block_of(t);
-        const int kvalid = j < 0 ? 0 : min(BS, L - j * BS);
+    for (int t = 0; t < ucnt; ++t) {
+        const char* cur = kbuf[t & 1];
+        if (t + 1 < ucnt) copy.issue_all(kg, (int)(ulist[t + 1] & 0xFFFF), L, kbuf[(t + 1) & 1], w, lane);
+        const uint32_t e = __builtin_amdgcn_readfirstlane(ulist[t]);
+        const int j = (int)(e & 0xFFFF);
+        const bool member = ((e >> (16 + g)) & 1u) != 0;
+        const int kvalid = min(BS, L - j * BS);
         int c = 0;
+        if (member) {
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt) {
-            f32x16 sv = f32x16{};
+            for (int rt = 0; rt < RT; ++rt) {
+                f32x16 sv = f32x16{};
 #pragma unroll
-            for (int kk = 0; kk < KK; ++kk) {
-                const bf16x8 a = __builtin_bit_cast(
-                    bf16x8, *reinterpret_cast<const uint4*>(cur + ((ka ^ (32 * kk)) + 32 * rt * ROWB)));
-                sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sv, 0, 0, 0);
+                for (int kk = 0; kk < KK; ++kk) {
+                    const bf16x8 a = __builtin_bit_cast(
+                        bf16x8, *reinterpret_cast<const uint4*>(cur + ((ka ^ (32 * kk)) + 32 * rt * ROWB)));
+                    sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sv, 0, 0, 0);
+                }
+                if (kvalid == BS) {
+#pragma unroll
+                    for (int ii = 0; ii < 16; ++ii) c += sv[ii] >= thr ? 1 : 0;
+                } else {
+                    // short tail tile: rows at or past the end of the sequence never count
+#pragma unroll
+                    for (int ii = 0; ii < 16; ++ii) {
+                        const int kv = 32 * rt + 8 * (ii >> 2) + 4 * h + (ii & 3);
+                        c += (kv < kvalid && sv[ii] >= thr) ? 1 : 0;
+                    }
+                }
             }
 #pragma unroll
-            for (int ii = 0; ii < 16; ++ii) {
-                const int kv = 32 * rt + 8 * (ii >> 2) + 4 * h + (ii & 3);
-                c += (kv < kvalid && sv[ii] * scale >= thr) ? 1 : 0;
-            }
+            for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
         }
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
-        if (lane == 0) part[t & 1][w] = c;
+        if (lane == 0) part[t & 1][g][qw] = c;
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
-        if (tid == 0 && j >= 0 && j < nv) {
+        if (member && qw == 0 && lane == 0 && i < nv && j < nv) {
             int total = 0;
 #pragma unroll
-            for (int ww = 0; ww < QW; ++ww) total += part[t & 1][ww];
+            for (int ww = 0; ww < QW; ++ww) total += part[t & 1][g][ww];
             stat[((size_t)bh * nv + i) * nv + j] = (double)total / ((double)rows_i * (double)kvalid);
         }
     }
@@ -857,7 +891,8 @@ template <int D, int BS>
 hipError_t launch_count(const uint16_t* q, const uint16_t* k, const int32_t* kv_idx, const int32_t* kv_cnt,
                         const float* lse, float scale, float log_eta, double* stat, int BH, int L, int n,
                         int nv, hipStream_t s) {
-    hipLaunchKernelGGL((stat_count_kernel<D, BS>), dim3((unsigned)BH * nv), dim3(BS * 2), 0, s, q, k, kv_idx,
+    const unsigned npv = (unsigned)(nv + 1) / 2;
+    hipLaunchKernelGGL((stat_count_kernel<D, BS>), dim3((unsigned)BH * npv), dim3(BS * 4), 0, s, q, k, kv_idx,
                        kv_cnt, lse, scale, log_eta, stat, L, n, nv);
     return hipGetLastError();
 }

@@ -2,7 +2,7 @@
 its block-level reconstruction (Eq. 5) through the C ABI.
 
 The count of probabilities reaching eta is an integer decided in floating
-point; the GPU decides in fp32 (scale * s >= lse + log eta) and the oracle in
+point; the GPU decides in fp32 (s >= (lse + log eta) / scale) and the oracle in
 fp64 against the GPU's own lse, so per block the counts may differ only by
 entries whose log-probability lies within TOL of log(eta).  The fit, the
 extrapolation and the selection are then checked against the oracle fed
