@@ -49,6 +49,31 @@ __device__ double block_max(double v, double* red) {
     return r;
 }
 
+// Exclusive scan over the 256 threads of a workgroup in thread order (a
+// wave scan, then the wave totals added in wave order: a fixed order).
+// wsum: kThreads / 64 entries of LDS scratch; *total receives the sum.
+template <class T>
+__device__ T block_exclusive_scan(T v, T* wsum, T* total) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    T incl = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const T y = __shfl_up(incl, off);
+        if (lane >= off) incl += y;
+    }
+    if (lane == 63) wsum[w] = incl;
+    __syncthreads();
+    T base = T(0), all = T(0);
+#pragma unroll
+    for (int ww = 0; ww < kThreads / 64; ++ww) {
+        if (ww < w) base += wsum[ww];
+        all += wsum[ww];
+    }
+    __syncthreads();   // wsum may be reused by the caller
+    *total = all;
+    return base + (incl - v);
+}
+
 // ---------------------------------------------------------------------------
 // a1: block pooling.  Grid (n, BH, 2): z = 0 pools Q, z = 1 pools K.  The
 // block is one contiguous run of rows*D bf16; each thread reads 16-byte
@@ -369,17 +394,27 @@ __device__ inline float order_bits_to_float(uint32_t k) {
     return __uint_as_float(u);
 }
 
+__device__ inline uint64_t shfl_xor_u64(uint64_t v, int mask) {
+    const uint32_t lo = __shfl_xor(static_cast<uint32_t>(v), mask);
+    const uint32_t hi = __shfl_xor(static_cast<uint32_t>(v >> 32), mask);
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// E = npad / kThreads keys per thread: thread t holds positions E*t .. E*t+E-1.
+template <int E>
 __global__ __launch_bounds__(kThreads) void select_kernel(
     const double* __restrict__ pred, const int32_t* __restrict__ gate,
     const int* __restrict__ row_lo, const int* __restrict__ row_hi, int mode, int topk,
-    double tau, int32_t* __restrict__ kv_idx, int32_t* __restrict__ kv_cnt, int n, int npad,
+    double tau, int32_t* __restrict__ kv_idx, int32_t* __restrict__ kv_cnt, int n,
     int ldn, int tb0) {
+    constexpr int npad = E * kThreads;
     extern __shared__ __align__(16) unsigned char smem[];
     uint64_t* keys = reinterpret_cast<uint64_t*>(smem);          // npad
     double* scan = reinterpret_cast<double*>(keys + npad);        // npad
     int* flag = reinterpret_cast<int*>(scan + npad);              // npad
     __shared__ double red[kThreads];
-    __shared__ int ired[kThreads];
+    __shared__ double wsum_d[kThreads / 64];
+    __shared__ int wsum_i[kThreads / 64];
     __shared__ int kk_shared;
 
     const int row = blockIdx.x;
@@ -396,7 +431,10 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     const int t = threadIdx.x;
 
     double forced_mass = 0.0;
-    for (int j = t; j < npad; j += kThreads) {
+    uint64_t kr[E];                  // this thread's keys (positions E*t + e)
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int j = E * t + e;
         uint64_t key = 0;
         int fl = 0;
         if (j < n) {
@@ -410,30 +448,63 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
                       static_cast<uint64_t>(0xFFFFFFFFu - static_cast<uint32_t>(j));
             }
         }
-        keys[j] = key;
+        kr[e] = key;
         flag[j] = fl;
     }
-    __syncthreads();
 
-    // descending bitonic sort of keys[0, npad)
+    // Descending bitonic sort of the npad keys.  Stage (kk, jj) pairs
+    // positions a and a ^ jj; the lower position of a pair keeps the larger
+    // key when (a & kk) == 0, the smaller one otherwise.  Partners within a
+    // thread (jj < E) are in its registers, within a wave (jj < 64 E) they
+    // are exchanged by cross-lane shuffles, and only the stages with partners
+    // in other waves go through LDS.
+#pragma unroll
     for (int kk = 2; kk <= npad; kk <<= 1) {
+#pragma unroll
         for (int jj = kk >> 1; jj > 0; jj >>= 1) {
-            for (int a = t; a < npad; a += kThreads) {
-                const int b = a ^ jj;
-                if (b > a) {
-                    const uint64_t ka = keys[a], kb = keys[b];
-                    const bool desc = (a & kk) == 0;
-                    if (desc ? (ka < kb) : (ka > kb)) {
-                        keys[a] = kb;
-                        keys[b] = ka;
+            if (jj < E) {
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    const int eb = e ^ jj;
+                    if (eb > e) {
+                        const int a = E * t + e;
+                        const bool desc = (a & kk) == 0;
+                        const uint64_t ka = kr[e], kb = kr[eb];
+                        const bool swap = desc ? (ka < kb) : (ka > kb);
+                        kr[e] = swap ? kb : ka;
+                        kr[eb] = swap ? ka : kb;
                     }
                 }
+            } else {
+                uint64_t pv[E];
+                if (jj < 64 * E) {
+#pragma unroll
+                    for (int e = 0; e < E; ++e) pv[e] = shfl_xor_u64(kr[e], jj / E);
+                } else {
+                    __syncthreads();     // the previous exchange has been read
+#pragma unroll
+                    for (int e = 0; e < E; ++e) keys[E * t + e] = kr[e];
+                    __syncthreads();
+#pragma unroll
+                    for (int e = 0; e < E; ++e) pv[e] = keys[(E * t + e) ^ jj];
+                }
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    const int a = E * t + e;
+                    const bool lower = (a & jj) == 0;
+                    const bool desc = (a & kk) == 0;
+                    const uint64_t hi = kr[e] > pv[e] ? kr[e] : pv[e];
+                    const uint64_t lo = kr[e] > pv[e] ? pv[e] : kr[e];
+                    kr[e] = (lower == desc) ? hi : lo;
+                }
             }
-            __syncthreads();
         }
     }
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < E; ++e) keys[E * t + e] = kr[e];
+    __syncthreads();
 
-    const int E = npad / kThreads;   // consecutive sorted positions per thread
     int keep;
     if (mode == 0) {
         keep = min(n_free, max(0, topk - nf));
@@ -452,18 +523,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
             run += v;
             scan[pos] = run;
         }
-        red[t] = run;
-        __syncthreads();
-        if (t == 0) {
-            double off = 0.0;
-            for (int a = 0; a < kThreads; ++a) {
-                const double v = red[a];
-                red[a] = off;
-                off += v;
-            }
-        }
-        __syncthreads();
-        const double off = red[t];
+        double unused;
+        const double off = block_exclusive_scan(run, wsum_d, &unused);
         for (int e = 0; e < E; ++e) scan[t * E + e] += off;
         if (t == 0) kk_shared = n_free;
         __syncthreads();
@@ -488,21 +549,9 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     // compaction in ascending j
     int cnt = 0;
     for (int e = 0; e < E; ++e) cnt += flag[t * E + e];
-    ired[t] = cnt;
-    __syncthreads();
-    if (t == 0) {
-        int off = 0;
-        for (int a = 0; a < kThreads; ++a) {
-            const int v = ired[a];
-            ired[a] = off;
-            off += v;
-        }
-        kk_shared = off;
-    }
-    __syncthreads();
-    const int total = kk_shared;
+    int total;
+    int pos = block_exclusive_scan(cnt, wsum_i, &total);
     const size_t orow = (size_t)bh * ldn + i;     // row of the [BH, ldn, ldn] lists
-    int pos = ired[t];
     int32_t* out = kv_idx + orow * ldn;
     for (int e = 0; e < E; ++e) {
         const int j = t * E + e;
@@ -705,17 +754,23 @@ hipError_t launch_select(const double* pred, const int32_t* gate, const int* row
     int npad = kThreads;
     while (npad < n) npad <<= 1;
     const size_t lds = (size_t)npad * (sizeof(uint64_t) + sizeof(double) + sizeof(int));
-    static bool attr_set = false;
-    if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_kernel),
+    auto go = [&](auto kern) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                            hipFuncAttributeMaxDynamicSharedMemorySize,
                                            (int)((size_t)kMaxBlocks * 20));
         if (e != hipSuccess) return e;
-        attr_set = true;
+        hipLaunchKernelGGL(kern, dim3((unsigned)BH * n), dim3(kThreads), lds, s, pred, gate, row_lo, row_hi,
+                           mode, k, tau, kv_idx, kv_cnt, n, ldn, tb0);
+        return hipGetLastError();
+    };
+    hipError_t e;
+    switch (npad / kThreads) {
+        case 1: e = go(select_kernel<1>); break;
+        case 2: e = go(select_kernel<2>); break;
+        case 4: e = go(select_kernel<4>); break;
+        case 8: e = go(select_kernel<8>); break;
+        default: e = go(select_kernel<16>); break;
     }
-    hipLaunchKernelGGL(select_kernel, dim3((unsigned)BH * n), dim3(kThreads), lds, s, pred, gate,
-                       row_lo, row_hi, mode, k, tau, kv_idx, kv_cnt, n, npad, ldn, tb0);
-    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_text_rows(kv_idx, kv_cnt, BH, ldn, tb0, s);
 }
