@@ -194,32 +194,61 @@ __global__ __launch_bounds__(kThreads) void mass_softmax_kernel(double* __restri
 
 // ---------------------------------------------------------------------------
 // a3 (rhs): r = M^T vec(G): diagonal sums (2n-1), column sums (n) and frame
-// square sums (F).  One thread per output, sequential in-order sums; the
-// diagonal and column loops read consecutive addresses across threads.
+// square sums (F).  Diagonals and columns: one thread per output, its
+// entries taken in row order into four interleaved partial sums (rows i mod
+// 4) combined as (s0 + s1) + (s2 + s3); consecutive threads read
+// consecutive addresses.  Frame squares: one work-group per (frame, head),
+// a fixed assignment of entries to threads and a fixed-order tree.  Every
+// sum has a fixed order, so the result is deterministic.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void rhs_kernel(const double* __restrict__ G,
-                                                       const int* __restrict__ reg,
                                                        double* __restrict__ r, int n, int F) {
     const int bh = blockIdx.y;
     const int o = blockIdx.x * kThreads + threadIdx.x;
     const int p = 3 * n - 1 + F;
-    if (o >= p) return;
+    if (o >= 3 * n - 1) return;
+    const double* g = G + (size_t)bh * n * n;
+    int i0, i1;
+    size_t step, at;
+    if (o < 2 * n - 1) {                 // diagonal j - i = dl
+        const int dl = o - (n - 1);
+        i0 = max(0, -dl);
+        i1 = min(n - 1, n - 1 - dl);
+        step = (size_t)n + 1;
+        at = (size_t)i0 * n + i0 + dl;
+    } else {                             // column j
+        i0 = 0;
+        i1 = n - 1;
+        step = (size_t)n;
+        at = (size_t)(o - (2 * n - 1));
+    }
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    int i = i0;
+    for (; i + 3 <= i1; i += 4, at += 4 * step) {
+        s0 += g[at];
+        s1 += g[at + step];
+        s2 += g[at + 2 * step];
+        s3 += g[at + 3 * step];
+    }
+    for (int q = 0; i <= i1; ++i, ++q, at += step) {
+        if (q == 0) s0 += g[at];
+        else if (q == 1) s1 += g[at];
+        else s2 += g[at];
+    }
+    r[(size_t)bh * p + o] = (s0 + s1) + (s2 + s3);
+}
+
+__global__ __launch_bounds__(kThreads) void rhs_frame_kernel(const double* __restrict__ G,
+                                                             const int* __restrict__ reg,
+                                                             double* __restrict__ r, int n, int F) {
+    __shared__ double red[kThreads];
+    const int f = blockIdx.x, bh = blockIdx.y;
+    const int lo = reg[2 * f], hi = reg[2 * f + 1], sz = hi - lo + 1;
     const double* g = G + (size_t)bh * n * n;
     double s = 0.0;
-    if (o < 2 * n - 1) {
-        const int dl = o - (n - 1);
-        const int i0 = max(0, -dl), i1 = min(n - 1, n - 1 - dl);
-        for (int i = i0; i <= i1; ++i) s += g[(size_t)i * n + i + dl];
-    } else if (o < 3 * n - 1) {
-        const int j = o - (2 * n - 1);
-        for (int i = 0; i < n; ++i) s += g[(size_t)i * n + j];
-    } else {
-        const int f = o - (3 * n - 1);
-        const int lo = reg[2 * f], hi = reg[2 * f + 1];
-        for (int i = lo; i <= hi; ++i)
-            for (int j = lo; j <= hi; ++j) s += g[(size_t)i * n + j];
-    }
-    r[(size_t)bh * p + o] = s;
+    for (int e = threadIdx.x; e < sz * sz; e += kThreads) s += g[(size_t)(lo + e / sz) * n + lo + e % sz];
+    s = block_sum(s, red);
+    if (threadIdx.x == 0) r[(size_t)bh * (3 * n - 1 + F) + 3 * n - 1 + f] = s;
 }
 
 // ---------------------------------------------------------------------------
@@ -239,13 +268,15 @@ __global__ __launch_bounds__(kThreads) void solve_pre_kernel(const double* __res
                                                              double* __restrict__ bU, int n,
                                                              int F) {
     extern __shared__ double y[];   // 2n - 1
-    const int bh = blockIdx.x;
+    const int bh = blockIdx.y;      // x: a chunk of kThreads outputs
     const int p = 3 * n - 1 + F, q = n - 1 + F;
     const double* rr = r + (size_t)bh * p;
     for (int a = threadIdx.x; a < 2 * n - 1; a += kThreads)
         y[a] = rr[a] / static_cast<double>(n - abs(a - (n - 1)));
     __syncthreads();
-    for (int j = threadIdx.x; j < q; j += kThreads) {
+    {
+        const int j = blockIdx.x * kThreads + threadIdx.x;
+        if (j >= q) return;
         double s = 0.0, b;
         if (j < n - 1) {
             for (int a = j; a <= j + n - 1; ++a) s += y[a];
@@ -303,15 +334,14 @@ __global__ __launch_bounds__(kThreads) void solve_post_kernel(const double* __re
                                                               double* __restrict__ X, int n,
                                                               int F) {
     extern __shared__ double us[];   // q
-    __shared__ double red[kThreads];
-    const int bh = blockIdx.x;
+    const int bh = blockIdx.y;       // x: a chunk of kThreads outputs of X
     const int p = 3 * n - 1 + F, q = n - 1 + F;
     for (int a = threadIdx.x; a < q; a += kThreads) us[a] = u[(size_t)bh * q + a];
     __syncthreads();
     const double* rr = r + (size_t)bh * p;
     double* x = X + (size_t)bh * p;
-    double part = 0.0;   // sum(c) - sum(d) of this thread's entries
-    for (int a = threadIdx.x; a < 2 * n - 1; a += kThreads) {
+    const int a = blockIdx.x * kThreads + threadIdx.x;
+    if (a < 2 * n - 1) {
         const int dl = a - (n - 1);
         double s = 0.0;
         const int j0 = max(0, dl), j1 = min(n - 2, dl + n - 1);
@@ -320,16 +350,23 @@ __global__ __launch_bounds__(kThreads) void solve_post_kernel(const double* __re
             const int w = (reg[2 * f + 1] - reg[2 * f] + 1) - abs(dl);
             if (w > 0) s += static_cast<double>(w) * us[n - 1 + f];
         }
-        const double c = (rr[a] - s) / static_cast<double>(n - abs(dl));
-        x[a] = c;
-        part += c;
+        x[a] = (rr[a] - s) / static_cast<double>(n - abs(dl));
+    } else if (a < 3 * n - 1) {
+        const int j = a - (2 * n - 1);
+        x[a] = (j < n - 1) ? us[j] : 0.0;
+    } else if (a < p) {
+        x[a] = us[n - 1 + (a - (3 * n - 1))];
     }
-    for (int j = threadIdx.x; j < n; j += kThreads) {
-        const double dj = (j < n - 1) ? us[j] : 0.0;
-        x[2 * n - 1 + j] = dj;
-        part -= dj;
-    }
-    for (int f = threadIdx.x; f < F; f += kThreads) x[3 * n - 1 + f] = us[n - 1 + f];
+}
+
+// Minimum-norm gauge: remove the component of X along z = [1, -1, 0].
+__global__ __launch_bounds__(kThreads) void solve_gauge_kernel(double* __restrict__ X, int n, int F) {
+    __shared__ double red[kThreads];
+    const int p = 3 * n - 1 + F;
+    double* x = X + (size_t)blockIdx.x * p;
+    double part = 0.0;   // sum(c) - sum(d) of this thread's entries
+    for (int a = threadIdx.x; a < 2 * n - 1; a += kThreads) part += x[a];
+    for (int j = threadIdx.x; j < n; j += kThreads) part -= x[2 * n - 1 + j];
     const double alpha = block_sum(part, red) / static_cast<double>(3 * n - 1);
     for (int a = threadIdx.x; a < 2 * n - 1; a += kThreads) x[a] -= alpha;
     for (int j = threadIdx.x; j < n; j += kThreads) x[2 * n - 1 + j] += alpha;
@@ -705,16 +742,17 @@ hipError_t launch_block_mass(const double* qbar, const double* kbar, double* G, 
 
 hipError_t launch_rhs(const double* G, const int* reg, double* r, int BH, int n, int F,
                       hipStream_t s) {
-    const int p = 3 * n - 1 + F;
-    hipLaunchKernelGGL(rhs_kernel, dim3(cdiv(p, kThreads), BH), dim3(kThreads), 0, s, G, reg, r,
-                       n, F);
+    hipLaunchKernelGGL(rhs_kernel, dim3(cdiv(3 * n - 1, kThreads), BH), dim3(kThreads), 0, s, G, r, n, F);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(rhs_frame_kernel, dim3(F, BH), dim3(kThreads), 0, s, G, reg, r, n, F);
     return hipGetLastError();
 }
 
 hipError_t launch_solve(const double* r, const int* reg, const double* Sinv, double* bU,
                         double* u, double* X, int BH, int n, int F, hipStream_t s) {
     const int q = n - 1 + F;
-    hipLaunchKernelGGL(solve_pre_kernel, dim3(BH), dim3(kThreads),
+    hipLaunchKernelGGL(solve_pre_kernel, dim3(cdiv(q, kThreads), BH), dim3(kThreads),
                        (size_t)(2 * n - 1) * sizeof(double), s, r, reg, bU, n, F);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -722,8 +760,11 @@ hipError_t launch_solve(const double* r, const int* reg, const double* Sinv, dou
                        s, Sinv, bU, u, q, BH);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(solve_post_kernel, dim3(BH), dim3(kThreads), (size_t)q * sizeof(double), s,
-                       r, u, reg, X, n, F);
+    hipLaunchKernelGGL(solve_post_kernel, dim3(cdiv(3 * n - 1 + F, kThreads), BH), dim3(kThreads),
+                       (size_t)q * sizeof(double), s, r, u, reg, X, n, F);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(solve_gauge_kernel, dim3(BH), dim3(kThreads), 0, s, X, n, F);
     return hipGetLastError();
 }
 
