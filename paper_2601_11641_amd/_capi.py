@@ -192,7 +192,7 @@ def mod_predict_block_mask(stats, q, k, step: int, budget: mod_budget, kv_idx, k
 
 
 def mod_attn_workspace_bytes(shape: mod_shape) -> int:
-    return int(_lib.mod_attn_workspace_bytes(ctypes.byref(shape)))
+    return int(_lib.mod_attn_workspace_bytes(_ref(shape)))
 
 
 def mod_block_sparse_attn_fwd(shape: mod_shape, q, k, v, kv_idx, kv_cnt, scale: float, o,

@@ -97,7 +97,12 @@ def test_attention_rejects_null_pointers_on_host(M):
 
 
 def test_workspace_size(M):
-    assert M.mod_attn_workspace_bytes(M.make_shape(1, 24, 118800, 128, 128, 3600)) >= 0
+    """The attention workspace holds the work plan: one int per (head, pair of
+    query blocks) plus per-head tables; 0 for an invalid shape."""
+    ws = M.mod_attn_workspace_bytes(M.make_shape(1, 24, 118800, 128, 128, 3600))
+    assert ws >= 4 * 24 * 465 and ws % 256 == 0 and ws < 64 * 1024
+    assert M.mod_attn_workspace_bytes(M.make_shape(1, 2, 1024, 96, 64, 256)) == 0
+    assert M.mod_attn_workspace_bytes(None) == 0
 
 
 def test_struct_layouts_match_the_header(M, tmp_path):

@@ -268,6 +268,59 @@ def test_attention_empty_and_single_rows():
     _check_attention(cfg, dev, host, rows)
 
 
+def test_attention_empty_pairs_and_uneven_work():
+    """Work items (pairs of query blocks) whose lists are both empty (no
+    tile at all), next to rows holding every block: the work plan spreads
+    items of very different cost, every item is processed once, and empty
+    pairs give O = 0, lse = -inf."""
+    cfg = RAGGED["d128b64"]          # n = 19: pairs (0,1) .. (16,17), (18)
+    host, dev = _inputs(cfg)
+    n = cfg.n
+    rows = []
+    for b in range(cfg.B):
+        hh = []
+        for h in range(cfg.H):
+            r = []
+            for i in range(n):
+                pair = i // 2
+                if (pair + h) % 3 == 0:
+                    r.append([])                       # both rows of the pair empty
+                elif (pair + h) % 3 == 1:
+                    r.append(list(range(n)))           # full rows
+                else:
+                    r.append(sorted({i, (i * 7 + h) % n}))
+            hh.append(r)
+        rows.append(hh)
+    _check_attention(cfg, dev, host, rows)
+
+
+def test_attention_workspace_is_checked():
+    """The attention call rejects a missing or too small workspace on the
+    host, before anything is enqueued."""
+    import ctypes
+    cfg = W.CONFIGS["tiny"]
+    _, dev = _inputs(cfg)
+    qd, kd, vd = dev
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    n = cfg.n
+    need = M.mod_attn_workspace_bytes(shape)
+    assert need >= 4 * (cfg.B * cfg.H * ((n + 1) // 2))
+    idx = torch.zeros((cfg.B, cfg.H, n, n), dtype=torch.int32, device="cuda")
+    cnt = torch.zeros((cfg.B, cfg.H, n), dtype=torch.int32, device="cuda")
+    o = torch.empty_like(qd)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    lib = M.raw_lib()
+    stream = torch.cuda.current_stream().cuda_stream
+    args = (ctypes.byref(shape), qd.data_ptr(), kd.data_ptr(), vd.data_ptr(), idx.data_ptr(), cnt.data_ptr(),
+            0.0, o.data_ptr(), None)
+    assert lib.mod_block_sparse_attn_fwd(*args, None, need, stream) == M.MOD_ERR_INVALID_ARG
+    assert lib.mod_block_sparse_attn_fwd(*args, ws.data_ptr(), need - 1, stream) == M.MOD_ERR_INVALID_ARG
+    assert lib.mod_block_sparse_attn_fwd(*args, ws.data_ptr() + 8, need, stream) == M.MOD_ERR_INVALID_ARG
+    assert lib.mod_block_sparse_attn_fwd(*args, ws.data_ptr(), need, stream) == M.MOD_OK
+    torch.cuda.synchronize()
+    assert (o.float() == 0).all()          # every row empty: O = 0
+
+
 def test_state_errors_on_device():
     cfg = W.CONFIGS["tiny"]
     _, dev = _inputs(cfg)
