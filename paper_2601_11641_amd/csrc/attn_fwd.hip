@@ -500,6 +500,8 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     auto mphase = [&](const char* Kt, const char* Vp, auto on_tag) __attribute__((always_inline)) {
         constexpr bool on = decltype(on_tag)::value;
         if constexpr (on) {
+            // the matrix phase issues first when both waves of a SIMD are ready
+            __builtin_amdgcn_s_setprio(1);
             constexpr int NS = RT * KK;
             constexpr int PF = 2;
             bf16x8 ak[NS], av[NS];
@@ -533,6 +535,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
             for (int rt = 0; rt < RT; ++rt) asm volatile("" : "+v"(sacc[rt]));
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) asm volatile("" : "+v"(oacc[dt]));
+            __builtin_amdgcn_s_setprio(0);
         }
     };
     // The M phase of a unit runs both products unless neither is needed
