@@ -1,8 +1,9 @@
 // Block-sparse attention forward for gfx950 (Eq. 1 with a block mask).
 //
-// One work-group per (head, pair of query blocks 2p, 2p+1) with 2 * BS/32
-// waves in two groups: group g owns query block 2p+g, wave qw of a group owns
-// 32 of its query rows.  Both groups walk the union of the two kv lists, so
+// One work item per (head, pair of query blocks 2p, 2p+1), processed by a
+// persistent work-group (one per compute unit, items fetched from a work
+// plan written before the launch) with 2 * BS/32 waves in two groups: group g
+// owns query block 2p+g, wave qw of a group owns 32 of its query rows.  Both groups walk the union of the two kv lists, so
 // every K/V tile brought into LDS serves both blocks (a tile missing from one
 // block's list costs that group nothing but the wait).  Every wave runs an
 // online softmax over whole tiles, half a tile (a "unit") at a time.
@@ -28,6 +29,7 @@
 #include "moddit_internal.h"
 
 #include <algorithm>
+#include <atomic>
 #include <type_traits>
 
 namespace moddit {
@@ -742,17 +744,20 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     }   // next item
 }
 
+// Persistent work-groups per launch: one per compute unit of the current
+// device (cached per device; the attribute query is a host call).
 int persistent_groups() {
-    static int cus = 0;
-    if (cus == 0) {
-        int dev = 0, c = 0;
-        if (hipGetDevice(&dev) == hipSuccess &&
-            hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && c > 0)
-            cus = c;
-        else
-            cus = 256;
+    constexpr int kMaxDevices = 64;
+    static std::atomic<int> cus[kMaxDevices];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+    int c = cus[dev].load(std::memory_order_relaxed);
+    if (c == 0) {
+        if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || c <= 0)
+            c = 256;
+        cus[dev].store(c, std::memory_order_relaxed);
     }
-    return cus;
+    return c;
 }
 
 template <int D, int BS>
