@@ -163,7 +163,8 @@ struct TileCopy {
 //          above kPlanMaxHeads heads);
 //   lists  per XCD, its ranges of all heads in that order, as a list of
 //          items bh * npairs + p, plus its length, start and a zeroed
-//          fetch counter.
+//          fetch counter; the list is then bucket-sorted by decreasing cost
+//          (lists longer than kPlanSortMax keep the head order).
 // The attention work-groups are persistent (one per CU): a work-group
 // fetches the next item of its XCD's list with an atomic counter and, once
 // that list is drained, of the other XCDs' lists, until all are drained.
@@ -171,6 +172,8 @@ struct TileCopy {
 constexpr int kPlanThreads = 256;
 constexpr int kPlanMaxHeads = 4096;
 constexpr int kPlanHdr = 32;          // ints: ctr[8], len[8], start[8], pad
+constexpr int kPlanSortMax = 8192;    // longer XCD lists keep the head order
+constexpr int kPlanBuckets = 512;
 
 struct Plan {
     int* ctr;       // [8] fetch counters
@@ -262,7 +265,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_order_kernel(void* ws, int 
 }
 
 // one work-group per XCD list
-__global__ __launch_bounds__(kPlanThreads) void plan_lists_kernel(void* ws, int BH, int n) {
+__global__ __launch_bounds__(kPlanThreads) void plan_lists_kernel(const int32_t* __restrict__ kv_cnt,
+                                                                  void* ws, int BH, int n) {
     __shared__ int xtot[kXcds];
     __shared__ int scan[kPlanThreads];
     const Plan pl(ws, BH);
@@ -310,6 +314,43 @@ __global__ __launch_bounds__(kPlanThreads) void plan_lists_kernel(void* ws, int 
         pl.len[x] = xtot[x];
         pl.start[x] = first;
         pl.ctr[x] = 0;
+    }
+    // Longest items first: a bucket sort of the list by decreasing cost
+    // (order within a bucket unspecified; the order only affects timing).
+    // The few items far above the rest (rows that keep every block) then
+    // start early instead of being left for the end of the launch.
+    const int len = xtot[x];
+    if (len > kPlanSortMax) return;
+    __shared__ int vals[kPlanSortMax];
+    __shared__ int cursor[kPlanBuckets];
+    int shift = 0;
+    while (((4 + 2 * n) >> shift) >= kPlanBuckets) ++shift;
+    auto bucket = [&](int item) {
+        const int h = item / npairs, p = item % npairs;
+        const size_t r0 = (size_t)h * n + 2 * p;
+        const int c = 4 + clamp_count(kv_cnt, r0, n) + (2 * p + 1 < n ? clamp_count(kv_cnt, r0 + 1, n) : 0);
+        return (kPlanBuckets - 1) - (c >> shift);          // descending cost
+    };
+    for (int bb = t; bb < kPlanBuckets; bb += kPlanThreads) cursor[bb] = 0;
+    __syncthreads();   // also: every item of the list has been written
+    for (int a = t; a < len; a += kPlanThreads) {
+        const int it = pl.items[first + a];
+        vals[a] = it;
+        atomicAdd(&cursor[bucket(it)], 1);
+    }
+    __syncthreads();
+    if (t == 0) {   // exclusive scan of the bucket sizes (kPlanBuckets entries)
+        int run = 0;
+        for (int bb = 0; bb < kPlanBuckets; ++bb) {
+            const int c = cursor[bb];
+            cursor[bb] = run;
+            run += c;
+        }
+    }
+    __syncthreads();
+    for (int a = t; a < len; a += kPlanThreads) {
+        const int it = vals[a];
+        pl.items[first + atomicAdd(&cursor[bucket(it)], 1)] = it;
     }
 }
 
@@ -767,7 +808,7 @@ hipError_t launch(const uint16_t* q, const uint16_t* k, const uint16_t* v, const
     hipLaunchKernelGGL(plan_split_kernel, dim3((unsigned)BH), dim3(kPlanThreads), 0, s, kv_cnt, ws, BH, n);
     hipLaunchKernelGGL(plan_order_kernel, dim3((unsigned)((BH + kPlanThreads - 1) / kPlanThreads)),
                        dim3(kPlanThreads), 0, s, ws, BH);
-    hipLaunchKernelGGL(plan_lists_kernel, dim3(kXcds), dim3(kPlanThreads), 0, s, ws, BH, n);
+    hipLaunchKernelGGL(plan_lists_kernel, dim3(kXcds), dim3(kPlanThreads), 0, s, kv_cnt, ws, BH, n);
     const long items = (long)BH * ((n + 1) / 2);
     const unsigned groups = (unsigned)std::min<long>(persistent_groups(), items);
     hipLaunchKernelGGL((attn_fwd_kernel<D, BS>), dim3(groups), dim3(BS * 4), 0, s,
