@@ -117,26 +117,28 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(const uint16_t* __restri
 }
 
 // ---------------------------------------------------------------------------
-// a2 (part 1): block logits scale * qbar_i . kbar_j, 64 x 64 tile per
-// workgroup, 4 x 4 outputs per thread, channels staged through LDS.
+// a2 (part 1): block logits scale * qbar_i . kbar_j, 128 x 128 tile per
+// workgroup, 8 x 8 outputs per thread (rows ty + 16u, columns tx + 16v),
+// channels staged through LDS 8 at a time; each output is one fp64 dot
+// product in channel order.
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(kThreads) void logits_kernel(const double* __restrict__ qbar,
                                                           const double* __restrict__ kbar,
                                                           double* __restrict__ G, int n,
                                                           double scale) {
-    constexpr int T = 64, KC = 16;
+    constexpr int T = 128, KC = 8, U = T / 16;
     __shared__ double qs[T][KC + 1];
     __shared__ double ks[T][KC + 1];
     const int bh = blockIdx.z, i0 = blockIdx.y * T, j0 = blockIdx.x * T;
     const double* qb = qbar + (size_t)bh * n * D;
     const double* kb = kbar + (size_t)bh * n * D;
     const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
-    double acc[4][4];
+    double acc[U][U];
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int a = 0; a < U; ++a)
 #pragma unroll
-        for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
+        for (int b = 0; b < U; ++b) acc[a][b] = 0.0;
     for (int d0 = 0; d0 < D; d0 += KC) {
         for (int e = threadIdx.x; e < T * KC; e += kThreads) {
             const int r = e / KC, c = e % KC;
@@ -146,25 +148,25 @@ __global__ __launch_bounds__(kThreads) void logits_kernel(const double* __restri
         __syncthreads();
 #pragma unroll
         for (int c = 0; c < KC; ++c) {
-            double a[4], b[4];
+            double a[U], b[U];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < U; ++u) {
                 a[u] = qs[ty + 16 * u][c];
                 b[u] = ks[tx + 16 * u][c];
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
+            for (int u = 0; u < U; ++u)
 #pragma unroll
-                for (int v = 0; v < 4; ++v) acc[u][v] = fma(a[u], b[v], acc[u][v]);
+                for (int v = 0; v < U; ++v) acc[u][v] = fma(a[u], b[v], acc[u][v]);
         }
         __syncthreads();
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < U; ++u) {
         const int i = i0 + ty + 16 * u;
         if (i >= n) continue;
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
+        for (int v = 0; v < U; ++v) {
             const int j = j0 + tx + 16 * v;
             if (j < n) G[((size_t)bh * n + i) * n + j] = scale * acc[u][v];
         }
@@ -728,7 +730,7 @@ hipError_t launch_pool(const uint16_t* q, const uint16_t* k, double* qbar, doubl
 
 hipError_t launch_block_mass(const double* qbar, const double* kbar, double* G, int BH,
                              int L, int d, int bs, int n, double scale, hipStream_t s) {
-    const dim3 grid(cdiv(n, 64), cdiv(n, 64), BH);
+    const dim3 grid(cdiv(n, 128), cdiv(n, 128), BH);
     if (d == 128)
         hipLaunchKernelGGL(logits_kernel<128>, grid, dim3(kThreads), 0, s, qbar, kbar, G, n, scale);
     else
