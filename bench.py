@@ -208,6 +208,22 @@ def summarize_counters(pmc_dir: str):
         "shader_clock_ghz": round(xcd_cycles / (a["_ns"] * 1e-9) / 1e9, 3),
         "duration_ms_under_profiler": round(a["_ns"] * 1e-6, 3),
     }
+    # the pooling kernel (a1) of the same step: HBM-bound, Q and K read once
+    pool = lambda k: "pool_kernel" in k   # noqa: E731
+    pc, pd = load("C", pool), load("D", pool)
+    if pc and pd:
+        import workloads as W
+        cfg = W.CONFIGS["hunyuan"]
+        alg = 2.0 * cfg.B * cfg.H * cfg.L * cfg.d * 2 + 2.0 * cfg.B * cfg.H * cfg.n * cfg.d * 8
+        pf, pw = pc["FETCH_SIZE"] * 1024.0 * fetch_scale, pd["WRITE_SIZE"] * 1024.0 * write_scale
+        ns = 0.5 * (pc["_ns"] + pd["_ns"])
+        out["pool_kernel"] = {
+            "algorithmic_bytes": round(alg), "hbm_fetch_bytes": round(pf), "hbm_write_bytes": round(pw),
+            "duration_us_under_profiler": round(ns * 1e-3, 1),
+            "algorithmic_GBps": round(alg / (ns * 1e-9) / 1e9, 1),
+            "measured_GBps": round((pf + pw) / (ns * 1e-9) / 1e9, 1),
+            "frac_of_8TBps": round(alg / (ns * 1e-9) / 8e12, 4),
+        }
     with open(COUNTER_SUMMARY, "w") as f:
         json.dump(out, f, indent=1)
         f.write("\n")
