@@ -3,10 +3,15 @@
 // One work item per (head, pair of query blocks 2p, 2p+1), processed by a
 // persistent work-group (one per compute unit, items fetched from a work
 // plan written before the launch) with 2 * BS/32 waves in two groups: group g
-// owns query block 2p+g, wave qw of a group owns 32 of its query rows.  Both groups walk the union of the two kv lists, so
-// every K/V tile brought into LDS serves both blocks (a tile missing from one
-// block's list costs that group nothing but the wait).  Every wave runs an
-// online softmax over whole tiles, half a tile (a "unit") at a time.
+// owns query block 2p+g, wave qw of a group owns 32 of its query rows.  The
+// union of the two kv lists is walked in two parts.  First the blocks in
+// both lists: every K/V tile brought into LDS serves both groups.  Then the
+// blocks in one list only, both groups at once: group 0 walks those of
+// block 2p while group 1 walks those of block 2p+1, each with its own
+// buffers, so neither group waits through a tile the other one alone needs.
+// Every wave runs an online softmax over whole tiles, half a tile (a "unit")
+// at a time; the order of the tiles does not change the result beyond
+// rounding.
 //
 // Per unit a wave has two phases:
 //   M  S^T (kv x q) = K . Q^T with v_mfma_f32_32x32x16_bf16 (a lane owns one
@@ -24,8 +29,10 @@
 // matrix products overlap the other wave's softmax.
 //
 // K and V tiles (BS x D bf16, row-major, 16-byte chunks XOR-swizzled per row)
-// are copied straight into LDS (global_load_lds_dwordx4) during the X phases,
-// two buffers each: group 0 copies K, group 1 copies V, one tile ahead.
+// are copied straight into LDS (global_load_lds_dwordx4) during the X phases:
+// in the shared part two buffers each, group 0 copying K and group 1 V one
+// tile ahead; in the exclusive part one K and one V buffer per group, which
+// copies its own tiles half a tile ahead.
 #include "moddit_internal.h"
 
 #include <algorithm>
@@ -148,7 +155,51 @@ struct TileCopy {
             for (int ii = 0; ii < IPW; ++ii) issue_one(gt, ii, tile, w);
         }
     }
+
+    // Half tiles (rows [hh*BS/2, (hh+1)*BS/2)): IPH copies per wave, the
+    // same LDS layout as the full tile.
+    static constexpr int IPH = IPW / 2;
+    static constexpr int CPH = IPH * NW;          // copies per half tile
+
+    __device__ __forceinline__ void issue_half_one(const char* gt, int hh, int ii, char* tile, int w) const {
+        static_assert(IPH % NV == 0, "a wave's first copy of a half must start a swizzle period");
+        const int ins = hh * CPH + w * IPH + ii;
+        lds_copy16(gt + (size_t)ins * 1024, voff[ii % NV], tile + ins * 1024);
+    }
+
+    // Start copying half hh of tile j: a full tile is returned as a source
+    // address for issue_half_one, a short one is issued at once (nullptr).
+    __device__ __forceinline__ const char* start_half(const uint16_t* __restrict__ g, int j, int L, char* tile,
+                                                      int hh, int w, int lane) const {
+        const int kvalid = min(BS, L - j * BS);
+        if (kvalid == BS) return reinterpret_cast<const char*>(g + (size_t)j * BS * D);
+#pragma unroll
+        for (int ii = 0; ii < IPH; ++ii) {
+            const int ins = hh * CPH + w * IPH + ii;
+            const int row = ins * RPI + lane / LPR;
+            const int chunk = (lane % LPR) ^ swz<D>(row);
+            const uint32_t off = (uint32_t)((j * BS + min(row, kvalid - 1)) * ROWB + chunk * 16);
+            lds_copy16(g, off, tile + ins * 1024);
+        }
+        return nullptr;
+    }
+
+    __device__ __forceinline__ void issue_half(const uint16_t* __restrict__ g, int j, int L, char* tile, int hh,
+                                               int w, int lane) const {
+        const char* gt = start_half(g, j, L, tile, hh, w, lane);
+        if (gt != nullptr) {
+#pragma unroll
+            for (int ii = 0; ii < IPH; ++ii) issue_half_one(gt, hh, ii, tile, w);
+        }
+    }
 };
+
+// s_waitcnt vmcnt(N): at most N vector memory operations of the wave still
+// outstanding (they complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
 
 // ---------------------------------------------------------------------------
 // Work plan.  The per-pair work (about the two rows' list lengths) varies
@@ -369,18 +420,13 @@ __device__ __forceinline__ int fetch_item(const Plan& pl, int x) {
     return -1;
 }
 
-// Union of the kv lists of rows row0 and row0 + 1 (the second only if has1)
-// of the [rows, n] lists, compacted in ascending j into ulist as
-// j | membership << 16 (bit 0: row0, bit 1: row0 + 1).  Counts are clamped to
-// [0, n] (a row never reads past its n entries), entries outside [0, n) are
-// ignored and a repeated entry counts once.  Every thread of the NT-thread
-// work-group calls it; ulist is complete after the caller's next barrier.
+// Membership bytes umask[j] of the kv lists of rows row0 and row0 + 1 (the
+// second only if has1) of the [rows, n] lists: bit 0 row0, bit 1 row0 + 1.
+// Counts are clamped to [0, n] (a row never reads past its n entries),
+// entries outside [0, n) are ignored and a repeated entry counts once.
 template <int NT>
-__device__ __forceinline__ int union_of_rows(const int32_t* __restrict__ kv_idx,
-                                             const int32_t* __restrict__ kv_cnt, size_t row0, bool has1,
-                                             int n, uint8_t* umask, uint32_t* ulist, int* wsum, int tid,
-                                             int lane, int w) {
-    constexpr int JPT = kMaxBlocks / NT;
+__device__ __forceinline__ void mark_rows(const int32_t* __restrict__ kv_idx, const int32_t* __restrict__ kv_cnt,
+                                          size_t row0, bool has1, int n, uint8_t* umask, int tid) {
     const int cnt0 = min(max(kv_cnt[row0], 0), n);
     const int cnt1 = has1 ? min(max(kv_cnt[row0 + 1], 0), n) : 0;
     const int32_t* list0 = kv_idx + row0 * n;
@@ -397,6 +443,18 @@ __device__ __forceinline__ int union_of_rows(const int32_t* __restrict__ kv_idx,
         if ((unsigned)j < (unsigned)n) umask[j] |= 2;
     }
     __syncthreads();
+}
+
+// Union of the two lists, compacted in ascending j into ulist as
+// j | membership << 16.  Every thread of the NT-thread work-group calls it;
+// ulist is complete after the caller's next barrier.
+template <int NT>
+__device__ __forceinline__ int union_of_rows(const int32_t* __restrict__ kv_idx,
+                                             const int32_t* __restrict__ kv_cnt, size_t row0, bool has1,
+                                             int n, uint8_t* umask, uint32_t* ulist, int* wsum, int tid,
+                                             int lane, int w) {
+    constexpr int JPT = kMaxBlocks / NT;
+    mark_rows<NT>(kv_idx, kv_cnt, row0, has1, n, umask, tid);
     // thread tid compacts entries [tid*JPT, +JPT) after a work-group scan
     int mine = 0;
 #pragma unroll
@@ -426,6 +484,73 @@ __device__ __forceinline__ int union_of_rows(const int32_t* __restrict__ kv_idx,
     return ucnt;
 }
 
+struct UnionParts {
+    int ns, na, nb;   // blocks in both lists, in row0's only, in row0 + 1's only
+};
+
+// The same union, partitioned: the blocks of both rows first, then those of
+// row0 only, then those of row0 + 1 only, each part in ascending j (entries
+// j | membership << 16 as above).  wsum holds 2 * NT/64 ints.
+template <int NT>
+__device__ __forceinline__ UnionParts union_parts(const int32_t* __restrict__ kv_idx,
+                                                  const int32_t* __restrict__ kv_cnt, size_t row0, bool has1,
+                                                  int n, uint8_t* umask, uint32_t* ulist, int* wsum, int tid,
+                                                  int lane, int w) {
+    constexpr int JPT = kMaxBlocks / NT;
+    mark_rows<NT>(kv_idx, kv_cnt, row0, has1, n, umask, tid);
+    // per thread: counts of the three kinds among entries [tid*JPT, +JPT);
+    // both and row0-only are packed in 16-bit fields (counts <= kMaxBlocks)
+    uint32_t mine01 = 0;
+    int mine2 = 0;
+#pragma unroll
+    for (int e = 0; e < JPT; ++e) {
+        const int j = tid * JPT + e;
+        const int u = j < n ? umask[j] : 0;
+        mine01 += u == 3 ? 1u : (u == 1 ? 0x10000u : 0u);
+        mine2 += u == 2 ? 1 : 0;
+    }
+    uint32_t inc01 = mine01;
+    int inc2 = mine2;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t y01 = __shfl_up(inc01, off);
+        const int y2 = __shfl_up(inc2, off);
+        if (lane >= off) {
+            inc01 += y01;
+            inc2 += y2;
+        }
+    }
+    if (lane == 63) {
+        wsum[2 * w] = (int)inc01;
+        wsum[2 * w + 1] = inc2;
+    }
+    __syncthreads();
+    uint32_t pos01 = inc01 - mine01, tot01 = 0;
+    int pos2 = inc2 - mine2, tot2 = 0;
+#pragma unroll
+    for (int ww = 0; ww < NT / 64; ++ww) {
+        pos01 += ww < w ? (uint32_t)wsum[2 * ww] : 0u;
+        pos2 += ww < w ? wsum[2 * ww + 1] : 0;
+        tot01 += (uint32_t)wsum[2 * ww];
+        tot2 += wsum[2 * ww + 1];
+    }
+    UnionParts r;
+    r.ns = (int)(tot01 & 0xFFFF);
+    r.na = (int)(tot01 >> 16);
+    r.nb = tot2;
+    int p3 = (int)(pos01 & 0xFFFF), p1 = r.ns + (int)(pos01 >> 16), p2 = r.ns + r.na + pos2;
+#pragma unroll
+    for (int e = 0; e < JPT; ++e) {
+        const int j = tid * JPT + e;
+        const int u = j < n ? umask[j] : 0;
+        const uint32_t ent = (uint32_t)j | ((uint32_t)u << 16);
+        if (u == 3) ulist[p3++] = ent;
+        if (u == 1) ulist[p1++] = ent;
+        if (u == 2) ulist[p2++] = ent;
+    }
+    return r;
+}
+
 template <int D, int BS>
 __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
@@ -449,7 +574,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     __shared__ __align__(1024) char vb1[TILE];
     __shared__ uint32_t ulist[kMaxBlocks];     // union of the two lists: j | membership << 16
     __shared__ uint8_t umask[kMaxBlocks];
-    __shared__ int wsum[NT / 64];
+    __shared__ int wsum[2 * NT / 64];
     __shared__ int item_s;
 
     // Persistent work-group on XCD blockIdx % 8 (dispatch order): items
@@ -478,9 +603,11 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     const float c2 = scale * kLog2e;
     const int qrow = i * BS + 32 * qw + l32;
 
-    // ---- union of the kv lists of blocks 2p and 2p+1, ascending j ----
+    // ---- union of the kv lists of blocks 2p and 2p+1: the ns blocks of
+    // both lists, then the na of block 2p's only, then the nb of 2p+1's only ----
     const size_t row0 = (size_t)bh * n + 2 * pr;
-    const int ucnt = union_of_rows<NT>(kv_idx, kv_cnt, row0, 2 * pr + 1 < n, n, umask, ulist, wsum, tid, lane, w);
+    const UnionParts parts = union_parts<NT>(kv_idx, kv_cnt, row0, 2 * pr + 1 < n, n, umask, ulist, wsum, tid, lane, w);
+    const int ns = parts.ns, na = parts.na, nb = parts.nb;
     // The first product (before any unit has been computed) multiplies a
     // zero P with the second half of the "previous" V buffer: that half
     // holds zeros rather than whatever the LDS held before.
@@ -603,7 +730,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     // or nullptr) into ct are interleaved with the fast path's exponentials
     // (the compiler schedules them), or issued at once by the slow path when
     // the fast path did not run.
-    auto exps = [&](auto copies_tag, const char* cgx, char* ct, float& ps0, float& ps1) __attribute__((always_inline)) {
+    auto exps = [&](auto copies_tag, auto&& cpf, float& ps0, float& ps1) __attribute__((always_inline)) {
         constexpr bool copies = decltype(copies_tag)::value;
         constexpr int NE = RT * 16;
         static_assert(NE % IPW == 0, "copies must spread evenly over the exponentials");
@@ -611,7 +738,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
         ps1 = 0.0f;
 #pragma unroll
         for (int qq = 0; qq < NE; ++qq) {
-            if (copies && qq % (NE / IPW) == 0) copy.issue_one(cgx, qq / (NE / IPW), ct, qw);
+            if (copies && qq % (NE / IPW) == 0) cpf(qq / (NE / IPW));
             const int rt = qq / 16, c1 = (qq / 8) % 2, e = qq % 8;
             const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[rt][8 * c1 + e], c2, -mb));
             pb[2 * rt + c1][e] = static_cast<__bf16>(p);
@@ -624,7 +751,8 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
 #pragma unroll
         for (int c = 0; c < 2 * RT; ++c) asm volatile("" : "+v"(pb[c]));
     };
-    auto xphase = [&](int kvalid, auto half_tag, const char* cg, char* ct) __attribute__((always_inline)) {
+    auto no_copy = [](int) {};
+    auto xphase = [&](int kvalid, auto half_tag, bool cp_on, auto&& cpf) __attribute__((always_inline)) {
         constexpr int half = decltype(half_tag)::value;
         if (kvalid < BS) {
             asm volatile("" ::: "memory");
@@ -640,14 +768,14 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
         float ps0, ps1;
         bool fast = __all(m > -INFINITY);
         if (fast) {
-            if (cg != nullptr)
-                exps(yes{}, cg, ct, ps0, ps1);
+            if (cp_on)
+                exps(yes{}, cpf, ps0, ps1);
             else
-                exps(std::false_type{}, nullptr, ct, ps0, ps1);
+                exps(std::false_type{}, no_copy, ps0, ps1);
             fast = !__any(!(ps0 + ps1 <= kSumLimit));
-        } else if (cg != nullptr) {
+        } else if (cp_on) {
 #pragma unroll
-            for (int ii = 0; ii < IPW; ++ii) copy.issue_one(cg, ii, ct, qw);
+            for (int c = 0; c < IPW; ++c) cpf(c);
         }
         if (!fast) {
             asm volatile("" ::: "memory");
@@ -680,7 +808,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
             }
             m = m_new;
             mb = m_new == -INFINITY ? 0.0f : m_new * c2;
-            exps(std::false_type{}, nullptr, ct, ps0, ps1);
+            exps(std::false_type{}, no_copy, ps0, ps1);
         }
         l += ps0 + ps1;
         asm volatile("" : "+v"(l), "+v"(m), "+v"(mb));
@@ -695,50 +823,40 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     // waits for it at the end of the tile (slot 4t+3); group 1 copies V(t+1)
     // into vp (last read in slot 4t+1) and waits for it at the end of its
     // next M phase (slot 4t+5).
-    uint32_t e_cur = ucnt > 0 ? ulist[0] : 0u;
-    uint32_t e_nxt = ucnt > 1 ? ulist[1] : 0u;
+    uint32_t e_cur = ns > 0 ? ulist[0] : 0u;
+    uint32_t e_nxt = ns > 1 ? ulist[1] : 0u;
     e_cur = __builtin_amdgcn_readfirstlane(e_cur);
     e_nxt = __builtin_amdgcn_readfirstlane(e_nxt);
-    if (ucnt > 0) copy.issue_all(g == 0 ? kg : vg, (int)(e_cur & 0xFFFF), L, g == 0 ? kb0 : vb0, qw, lane);
+    if (ns > 0) copy.issue_all(g == 0 ? kg : vg, (int)(e_cur & 0xFFFF), L, g == 0 ? kb0 : vb0, qw, lane);
     wait_copies();
     barrier();
     if (g == 1) barrier();   // group 1 starts one phase late
 
     bool prev_active = false;   // the previous tile is in this group's list
+    // Every block of this part is in both lists: both groups run every phase
+    // (the first product multiplies P = 0).
     auto tile = [&](int t, char* kc, char* kn, char* vc, char* vp) __attribute__((always_inline)) {
-        const bool more = t + 1 < ucnt;
+        const bool more = t + 1 < ns;
         const int jc = (int)(e_cur & 0xFFFF), jn = (int)(e_nxt & 0xFFFF);
-        const bool active = ((e_cur >> (16 + g)) & 1u) != 0;
         const int kvalid = min(BS, L - jc * BS);
         // first half: S from K(t) rows [0, KVW); product of V(t-1) rows [KVW, BS)
-        mphase_if(kc, vp + HALF, active, prev_active);
+        mphase(kc, vp + HALF, yes{});
         if (g == 1) wait_copies();
         barrier();
         // copy of the next tile (a short one is issued at once by start())
         char* ct = g == 0 ? kn : vp;
         const char* cg = more ? copy.start(g == 0 ? kg : vg, jn, L, ct, qw, lane) : nullptr;
-        if (active) {
-            xphase(kvalid, std::integral_constant<int, 0>{}, cg, ct);
-        } else {
-            zero_p();
-            if (cg != nullptr) {
-#pragma unroll
-                for (int ii = 0; ii < IPW; ++ii) copy.issue_one(cg, ii, ct, qw);
-            }
-        }
+        xphase(kvalid, std::integral_constant<int, 0>{}, cg != nullptr,
+               [&](int c) __attribute__((always_inline)) { copy.issue_one(cg, c, ct, qw); });
         barrier();
         // second half: S from K(t) rows [KVW, BS); product of V(t) rows [0, KVW)
-        mphase_if(kc + HALF, vc, active, active);
+        mphase(kc + HALF, vc, yes{});
         barrier();
-        uint32_t e_after = t + 2 < ucnt ? ulist[t + 2] : 0u;
+        uint32_t e_after = t + 2 < ns ? ulist[t + 2] : 0u;
         e_after = __builtin_amdgcn_readfirstlane(e_after);
-        if (active)
-            xphase(kvalid, std::integral_constant<int, 1>{}, nullptr, ct);
-        else
-            zero_p();
+        xphase(kvalid, std::integral_constant<int, 1>{}, false, no_copy);
         if (g == 0) wait_copies();
         barrier();
-        prev_active = active;
         e_cur = e_nxt;
         e_nxt = e_after;
     };
@@ -748,7 +866,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     char* kn = kb1;
     char* vc = vb0;
     char* vp = vb1;
-    for (int t = 0; t < ucnt; ++t) {
+    for (int t = 0; t < ns; ++t) {
         tile(t, kc, kn, vc, vp);
         char* tmp = kc;
         kc = kn;
@@ -758,8 +876,108 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
         vp = tmp;
     }
     // the pending product of the last tile's second half (its V now in vp)
-    if (prev_active) mphase(kc, vp + HALF, yes{});
+    if (ns > 0) mphase(kc, vp + HALF, yes{});
     if (g == 0) barrier();   // both groups pass the same number of barriers
+
+    // ---- blocks in one list only: both groups at once ----
+    // Group 0 walks the na blocks of block 2p's list only and group 1 the nb
+    // of block 2p+1's only, in the same phase schedule (group 1 one phase
+    // behind).  Each group has its own buffers (group 0: kb0, vb0; group 1:
+    // kb1, vb1) and copies its own tiles half a tile ahead: during X of the
+    // first unit of tile x it copies K(x+1) rows [0, KVW) into the half that
+    // unit's M phase has released and V(x) rows [KVW, BS); during X of the
+    // second unit, K(x+1) rows [KVW, BS) and V(x+1) rows [0, KVW).  A group
+    // waits for its copies at the end of its next X phase.
+    const int ce = max(na, nb);   // work-group uniform
+    if (ce > 0) {
+        barrier();   // group 1's last product of the shared part has read its buffers
+        const int cgx = g == 0 ? na : nb;
+        const uint32_t* el = ulist + (g == 0 ? ns : ns + na);
+        char* kbuf = g == 0 ? kb0 : kb1;
+        char* vbuf = g == 0 ? vb0 : vb1;
+        constexpr int IPH = Copy::IPH;
+        zero_p();
+        uint32_t ec = cgx > 0 ? el[0] : 0u;
+        uint32_t en = cgx > 1 ? el[1] : 0u;
+        ec = __builtin_amdgcn_readfirstlane(ec);
+        en = __builtin_amdgcn_readfirstlane(en);
+        if (cgx > 0) {
+            // the first product multiplies P = 0 with this half: zeros, not stale LDS
+            for (int e = 64 * qw + lane; e < HALF / 16; e += 64 * QW)
+                reinterpret_cast<uint4*>(vbuf + HALF)[e] = make_uint4(0, 0, 0, 0);
+            copy.issue_all(kg, (int)(ec & 0xFFFF), L, kbuf, qw, lane);
+            copy.issue_half(vg, (int)(ec & 0xFFFF), L, vbuf, 0, qw, lane);
+        }
+        wait_copies();
+        barrier();
+        if (g == 1) barrier();   // group 1 starts one phase late
+        prev_active = false;
+        // Issue this X phase's copies (K half hk of tile jk if kon, V half hv
+        // of tile jv if von) interleaved with its exponentials, or at once if
+        // there is no softmax step or a copy is of a short tile; returns the
+        // number of copies the wave issued.
+        auto xcopies = [&](int kvalid, auto half_tag, bool active, bool kon, int jk, int hk, bool von, int jv,
+                           int hv) __attribute__((always_inline)) {
+            const char* sk = kon ? copy.start_half(kg, jk, L, kbuf, hk, qw, lane) : nullptr;
+            const char* sv = von ? copy.start_half(vg, jv, L, vbuf, hv, qw, lane) : nullptr;
+            const bool both = sk != nullptr && sv != nullptr;
+            if (!both || !active) {
+                if (sk != nullptr) {
+#pragma unroll
+                    for (int ii = 0; ii < IPH; ++ii) copy.issue_half_one(sk, hk, ii, kbuf, qw);
+                }
+                if (sv != nullptr) {
+#pragma unroll
+                    for (int ii = 0; ii < IPH; ++ii) copy.issue_half_one(sv, hv, ii, vbuf, qw);
+                }
+            }
+            if (active)
+                xphase(kvalid, half_tag, both, [&](int c) __attribute__((always_inline)) {
+                    if (c < IPH)
+                        copy.issue_half_one(sk, hk, c, kbuf, qw);
+                    else
+                        copy.issue_half_one(sv, hv, c - IPH, vbuf, qw);
+                });
+            else
+                zero_p();
+            return (kon ? IPH : 0) + (von ? IPH : 0);
+        };
+        // wait for the copies of the previous X phase: those of this one
+        // (issued later, completing later) may still be outstanding
+        auto wait_prev = [&](int issued) __attribute__((always_inline)) {
+            if (issued == 0)
+                wait_vmcnt<0>();
+            else if (issued == IPH)
+                wait_vmcnt<IPH>();
+            else
+                wait_vmcnt<2 * IPH>();
+        };
+        for (int x = 0; x < ce; ++x) {
+            const bool active = x < cgx;
+            const bool more = x + 1 < cgx;
+            const int jc = (int)(ec & 0xFFFF), jn = (int)(en & 0xFFFF);
+            const int kvalid = min(BS, L - jc * BS);
+            // first half: S from K(x) rows [0, KVW); product of V(x-1) rows [KVW, BS)
+            mphase_if(kbuf, vbuf + HALF, active, prev_active);
+            barrier();
+            const int n0 = xcopies(kvalid, std::integral_constant<int, 0>{}, active, more, jn, 0, active, jc, 1);
+            wait_prev(n0);
+            barrier();
+            // second half: S from K(x) rows [KVW, BS); product of V(x) rows [0, KVW)
+            mphase_if(kbuf + HALF, vbuf, active, active);
+            barrier();
+            uint32_t ea = x + 2 < cgx ? el[x + 2] : 0u;
+            ea = __builtin_amdgcn_readfirstlane(ea);
+            const int n1 = xcopies(kvalid, std::integral_constant<int, 1>{}, active, more, jn, 1, more, jn, 0);
+            wait_prev(n1);
+            barrier();
+            prev_active = active;
+            ec = en;
+            en = ea;
+        }
+        if (prev_active) mphase(kbuf, vbuf + HALF, yes{});
+        if (g == 0) barrier();
+    }
 
     // ---- output: this wave owns 32 complete query rows ----
     l += __shfl_xor(l, 32);

@@ -294,6 +294,45 @@ def test_attention_empty_pairs_and_uneven_work():
     _check_attention(cfg, dev, host, rows)
 
 
+@pytest.mark.parametrize("name", sorted(RAGGED))
+def test_attention_exclusive_blocks(name):
+    """Pairs of query blocks whose lists share some, all or none of their
+    blocks, with the blocks in one list only split evenly or unevenly
+    between the two rows, one row empty, and the short tail block in one
+    list only: the kernel walks the shared blocks with both rows and the
+    others with each row on its own (odd n leaves a last row unpaired)."""
+    cfg = RAGGED[name]
+    host, dev = _inputs(cfg)
+    n = cfg.n
+    rng = np.random.default_rng(1234 + n)
+    rows = []
+    for b in range(cfg.B):
+        hh = []
+        for h in range(cfg.H):
+            r = [None] * n
+            for p in range(0, n, 2):
+                kind = (p // 2 + h + b) % 5
+                perm = rng.permutation(n).tolist()
+                if kind == 0:      # identical lists
+                    a = c = perm[: max(1, n // 3)]
+                elif kind == 1:    # disjoint, equal sizes
+                    k = max(1, n // 4)
+                    a, c = perm[:k], perm[k:2 * k]
+                elif kind == 2:    # disjoint, uneven: row 2p has most
+                    a, c = perm[: max(1, n - 2)], perm[max(1, n - 2):]
+                elif kind == 3:    # overlap; the tail block in row 2p's list only
+                    a = sorted(set(perm[: n // 2]) | {n - 1})
+                    c = sorted(set(perm[n // 4: 3 * n // 4]) - {n - 1})
+                else:              # row 2p empty
+                    a, c = [], perm[: max(1, n // 2)]
+                r[p] = sorted(a)
+                if p + 1 < n:
+                    r[p + 1] = sorted(c)
+            hh.append(r)
+        rows.append(hh)
+    _check_attention(cfg, dev, host, rows)
+
+
 def test_attention_workspace_is_checked():
     """The attention call rejects a missing or too small workspace on the
     host, before anything is enqueued."""
