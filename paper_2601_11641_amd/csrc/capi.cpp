@@ -344,7 +344,7 @@ mod_status mod_stats_create(const mod_shape* shape, const mod_params* params, mo
         {(void**)&s->G, BH * n * n * sizeof(double)},
         {(void**)&s->r, BH * s->p * sizeof(double)},
         {(void**)&s->bU, BH * s->q * sizeof(double)},
-        {(void**)&s->u, BH * s->q * sizeof(double)},
+        {(void**)&s->u, (size_t)moddit::kSolveSplit * BH * s->q * sizeof(double)},   // per-chunk partial products
         {(void**)&s->X[0], BH * s->p * sizeof(double)},
         {(void**)&s->X[1], BH * s->p * sizeof(double)},
         {(void**)&s->pred, BH * (3 * n - 1) * sizeof(double)},

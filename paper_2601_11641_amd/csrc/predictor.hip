@@ -294,39 +294,37 @@ __global__ __launch_bounds__(kThreads) void solve_pre_kernel(const double* __res
     }
 }
 
-// u[h] = S^{-1} bU[h] for all heads; S^{-1} symmetric, read row-wise so that
-// consecutive threads read consecutive addresses.
+// u[h] = S^{-1} bU[h] for all heads, split over kSolveSplit fixed chunks of
+// k: part[c][h][j] = sum over k in chunk c (ascending) of S^{-1}[k][j] bU[h][k]
+// (S^{-1} symmetric, read row-wise: a wave's lanes read 64 consecutive
+// columns).  The post kernel adds the chunks in order, so the result does
+// not depend on the launch.  Grid: (column chunks of 64, kSolveSplit); wave
+// w takes heads w*8.. in passes of 32.
 __global__ __launch_bounds__(kThreads) void solve_gemv_kernel(const double* __restrict__ Sinv,
                                                               const double* __restrict__ bU,
-                                                              double* __restrict__ u, int q,
+                                                              double* __restrict__ part, int q,
                                                               int BH) {
-    constexpr int HB = 4, KT = 1024;
-    __shared__ double bs[HB][KT];
-    const int j = blockIdx.x * kThreads + threadIdx.x;
-    const int h0 = blockIdx.y * HB;
-    double acc[HB];
+    constexpr int HW = 8;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int j = blockIdx.x * 64 + lane;
+    const int c = blockIdx.y;
+    const int kc = (q + kSolveSplit - 1) / kSolveSplit;
+    const int k0 = min(q, c * kc), k1 = min(q, k0 + kc);
+    for (int h0 = w * HW; h0 < BH; h0 += (kThreads / 64) * HW) {
+        double acc[HW];
 #pragma unroll
-    for (int hh = 0; hh < HB; ++hh) acc[hh] = 0.0;
-    for (int k0 = 0; k0 < q; k0 += KT) {
-        const int kt = min(KT, q - k0);
-        for (int e = threadIdx.x; e < HB * KT; e += kThreads) {
-            const int hh = e / KT, kk = e % KT;
-            bs[hh][kk] = (h0 + hh < BH && kk < kt) ? bU[(size_t)(h0 + hh) * q + k0 + kk] : 0.0;
-        }
-        __syncthreads();
+        for (int hh = 0; hh < HW; ++hh) acc[hh] = 0.0;
         if (j < q) {
-            for (int kk = 0; kk < kt; ++kk) {
-                const double a = Sinv[(size_t)(k0 + kk) * q + j];
+            for (int k = k0; k < k1; ++k) {
+                const double a = Sinv[(size_t)k * q + j];
 #pragma unroll
-                for (int hh = 0; hh < HB; ++hh) acc[hh] = fma(a, bs[hh][kk], acc[hh]);
+                for (int hh = 0; hh < HW; ++hh)
+                    if (h0 + hh < BH) acc[hh] = fma(a, bU[(size_t)(h0 + hh) * q + k], acc[hh]);
             }
-        }
-        __syncthreads();
-    }
-    if (j < q) {
 #pragma unroll
-        for (int hh = 0; hh < HB; ++hh)
-            if (h0 + hh < BH) u[(size_t)(h0 + hh) * q + j] = acc[hh];
+            for (int hh = 0; hh < HW; ++hh)
+                if (h0 + hh < BH) part[((size_t)c * BH + h0 + hh) * q + j] = acc[hh];
+        }
     }
 }
 
@@ -334,11 +332,16 @@ __global__ __launch_bounds__(kThreads) void solve_post_kernel(const double* __re
                                                               const double* __restrict__ u,
                                                               const int* __restrict__ reg,
                                                               double* __restrict__ X, int n,
-                                                              int F) {
+                                                              int F, int BH) {
     extern __shared__ double us[];   // q
     const int bh = blockIdx.y;       // x: a chunk of kThreads outputs of X
     const int p = 3 * n - 1 + F, q = n - 1 + F;
-    for (int a = threadIdx.x; a < q; a += kThreads) us[a] = u[(size_t)bh * q + a];
+    // u = sum of the k-chunk partial products, in chunk order
+    for (int a = threadIdx.x; a < q; a += kThreads) {
+        double v = 0.0;
+        for (int c = 0; c < kSolveSplit; ++c) v += u[((size_t)c * BH + bh) * q + a];
+        us[a] = v;
+    }
     __syncthreads();
     const double* rr = r + (size_t)bh * p;
     double* x = X + (size_t)bh * p;
@@ -758,12 +761,12 @@ hipError_t launch_solve(const double* r, const int* reg, const double* Sinv, dou
                        (size_t)(2 * n - 1) * sizeof(double), s, r, reg, bU, n, F);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(solve_gemv_kernel, dim3(cdiv(q, kThreads), cdiv(BH, 4)), dim3(kThreads), 0,
-                       s, Sinv, bU, u, q, BH);
+    hipLaunchKernelGGL(solve_gemv_kernel, dim3(cdiv(q, 64), kSolveSplit), dim3(kThreads), 0, s, Sinv, bU,
+                       u, q, BH);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(solve_post_kernel, dim3(cdiv(3 * n - 1 + F, kThreads), BH), dim3(kThreads),
-                       (size_t)q * sizeof(double), s, r, u, reg, X, n, F);
+                       (size_t)q * sizeof(double), s, r, u, reg, X, n, F, BH);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(solve_gauge_kernel, dim3(BH), dim3(kThreads), 0, s, X, n, F);
