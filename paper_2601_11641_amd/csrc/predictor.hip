@@ -117,60 +117,84 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(const uint16_t* __restri
 }
 
 // ---------------------------------------------------------------------------
-// a2 (part 1): block logits scale * qbar_i . kbar_j, 128 x 128 tile per
-// workgroup, 8 x 8 outputs per thread (rows ty + 16u, columns tx + 16v),
-// channels staged through LDS 8 at a time; each output is one fp64 dot
-// product in channel order.
+// a2 (part 1): block logits scale * qbar_i . kbar_j with fp64 matrix
+// products (v_mfma_f64_16x16x4_f64): a 128 x 128 tile per work-group, 64 x 64
+// per wave (4 x 4 product tiles of 16 x 16), channels staged through LDS 16
+// at a time.  Operand layout of the product (16 x 4 times 4 x 16): lane l
+// supplies A[l % 16][l / 16] and B[l / 16][l % 16], and holds D[l / 16 + 4 e]
+// [l % 16] in element e of its result.
 // ---------------------------------------------------------------------------
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
 template <int D>
 __global__ __launch_bounds__(kThreads) void logits_kernel(const double* __restrict__ qbar,
                                                           const double* __restrict__ kbar,
                                                           double* __restrict__ G, int n,
                                                           double scale) {
-    constexpr int T = 128, KC = 8, U = T / 16;
+    constexpr int T = 128, KC = 16;
+    static_assert(D % KC == 0 && kThreads == 256, "four waves, 16-channel chunks");
     __shared__ double qs[T][KC + 1];
     __shared__ double ks[T][KC + 1];
     const int bh = blockIdx.z, i0 = blockIdx.y * T, j0 = blockIdx.x * T;
     const double* qb = qbar + (size_t)bh * n * D;
     const double* kb = kbar + (size_t)bh * n * D;
-    const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
-    double acc[U][U];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int wr = (w >> 1) * 64, wc = (w & 1) * 64;   // the wave's 64 x 64 sub-tile
+    const int lm = lane & 15, lk = lane >> 4;
+    f64x4 acc[4][4];
 #pragma unroll
-    for (int a = 0; a < U; ++a)
+    for (int u = 0; u < 4; ++u)
 #pragma unroll
-        for (int b = 0; b < U; ++b) acc[a][b] = 0.0;
+        for (int v = 0; v < 4; ++v) acc[u][v] = f64x4{0.0, 0.0, 0.0, 0.0};
+    // the next chunk is loaded into registers while this one is multiplied
+    constexpr int PT = T * KC / kThreads;   // values of each operand per thread
+    double qn[PT], kn[PT];
+    auto fetch = [&](int d0) {
+#pragma unroll
+        for (int x = 0; x < PT; ++x) {
+            const int e = threadIdx.x + x * kThreads, r = e / KC, c = e % KC;
+            qn[x] = (i0 + r < n) ? qb[(size_t)(i0 + r) * D + d0 + c] : 0.0;
+            kn[x] = (j0 + r < n) ? kb[(size_t)(j0 + r) * D + d0 + c] : 0.0;
+        }
+    };
+    fetch(0);
     for (int d0 = 0; d0 < D; d0 += KC) {
-        for (int e = threadIdx.x; e < T * KC; e += kThreads) {
-            const int r = e / KC, c = e % KC;
-            qs[r][c] = (i0 + r < n) ? qb[(size_t)(i0 + r) * D + d0 + c] : 0.0;
-            ks[r][c] = (j0 + r < n) ? kb[(size_t)(j0 + r) * D + d0 + c] : 0.0;
+#pragma unroll
+        for (int x = 0; x < PT; ++x) {
+            const int e = threadIdx.x + x * kThreads, r = e / KC, c = e % KC;
+            qs[r][c] = qn[x];
+            ks[r][c] = kn[x];
         }
         __syncthreads();
+        if (d0 + KC < D) fetch(d0 + KC);
 #pragma unroll
-        for (int c = 0; c < KC; ++c) {
-            double a[U], b[U];
+        for (int kk = 0; kk < KC; kk += 4) {
+            double a[4], b[4];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                a[u] = qs[ty + 16 * u][c];
-                b[u] = ks[tx + 16 * u][c];
+            for (int u = 0; u < 4; ++u) {
+                a[u] = qs[wr + 16 * u + lm][kk + lk];
+                b[u] = ks[wc + 16 * u + lm][kk + lk];
             }
 #pragma unroll
-            for (int u = 0; u < U; ++u)
+            for (int u = 0; u < 4; ++u)
 #pragma unroll
-                for (int v = 0; v < U; ++v) acc[u][v] = fma(a[u], b[v], acc[u][v]);
+                for (int v = 0; v < 4; ++v)
+                    acc[u][v] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[u], b[v], acc[u][v], 0, 0, 0);
         }
         __syncthreads();
     }
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int i = i0 + ty + 16 * u;
-        if (i >= n) continue;
+    for (int u = 0; u < 4; ++u)
 #pragma unroll
-        for (int v = 0; v < U; ++v) {
-            const int j = j0 + tx + 16 * v;
-            if (j < n) G[((size_t)bh * n + i) * n + j] = scale * acc[u][v];
+        for (int e = 0; e < 4; ++e) {
+            const int i = i0 + wr + 16 * u + lk + 4 * e;
+            if (i >= n) continue;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int j = j0 + wc + 16 * v + lm;
+                if (j < n) G[((size_t)bh * n + i) * n + j] = scale * acc[u][v][e];
+            }
         }
-    }
 }
 
 // ---------------------------------------------------------------------------
