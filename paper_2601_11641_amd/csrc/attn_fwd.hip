@@ -75,26 +75,31 @@ __device__ __forceinline__ void lds_copy16(const void* sbase, uint32_t voff, con
                  :: "v"(voff), "s"(sbase), "s"(m0) : "memory");
 }
 
-// XOR pattern applied to the 16-byte chunk index of a tile row.  The MFMA
-// operand loads read one chunk column of 8 (or 16) consecutive rows at a
-// time, so the pattern must differ in its low 3 (4) bits over any 8 (16)
-// aligned consecutive rows; the transposing loads read two adjacent chunks
-// (an even/odd pair) of 4 aligned consecutive rows, so bits 1..2 must differ
-// over any 4 such rows.  swz(r) = (r&3)<<1 | (r>>2)&1 | (r&8) meets both.
+// XOR pattern applied to the 16-byte chunk index of a tile row.  The LDS
+// serves 256 bytes (64 four-byte banks) per cycle: 16 lanes of a 16-byte
+// read, 32 lanes of an 8-byte read.  The MFMA operand loads (16 bytes per
+// lane) read one chunk column of 16 aligned consecutive rows per cycle, so
+// the pattern must be a permutation over any 16 such rows.  The transposing
+// loads (8 bytes per lane) read, per 32 lanes, the same four chunks (64
+// bytes) of 4 aligned consecutive rows, so over any such 4 rows the pattern
+// must differ in bits 2..3 (the 64-byte quarter of the row).  At D = 128,
+// swz(r) = (r&3)<<2 | (r>>2)&3 meets both.  At D = 64 a row (8 chunks)
+// covers half the banks and rows of either parity the other half, so the
+// conditions hold separately for the even and the odd rows:
+// swz(r) = ((r>>1)&1)<<2 | (r>>2)&3.
 template <int D>
 __device__ __forceinline__ int swz(int row) {
-    const int f = ((row & 3) << 1) | ((row >> 2) & 1);
     if constexpr (D == 128)
-        return f | (row & 8);
+        return ((row & 3) << 2) | ((row >> 2) & 3);
     else
-        return f;
+        return (((row >> 1) & 1) << 2) | ((row >> 2) & 3);
 }
 
 // A group's direct-to-LDS copies of one BS x D tile (NW waves, IPW 1-KB
 // copies each).  Copy `ins` fills LDS bytes [ins*1024, +1024): lane l writes
 // the 16-byte chunk at ins*1024 + 16*l, i.e. row ins*RPI + l/LPR, physical
 // chunk l % LPR, which holds logical chunk (l % LPR) ^ swz(row).  The
-// per-lane source offset only depends on ins mod 4 (D = 128) or not at all
+// per-lane source offset only depends on ins mod 4 (D = 128) or ins mod 2
 // (D = 64); it is precomputed in voff.  Rows past the end of the sequence
 // (short tail tile) re-read the last valid row: their scores are masked and
 // their probabilities are zero.
@@ -104,7 +109,7 @@ struct TileCopy {
     static constexpr int LPR = ROWB / 16;         // lanes per row
     static constexpr int RPI = 64 / LPR;          // rows per 1-KB copy
     static constexpr int IPW = BS * ROWB / 1024 / NW;
-    static constexpr int NV = D == 128 ? 4 : 1;
+    static constexpr int NV = D == 128 ? 4 : 2;
     uint32_t voff[NV];                             // byte offsets, lane part
 
     __device__ __forceinline__ explicit TileCopy(int lane) {
