@@ -197,7 +197,7 @@ mod_status mod_predict_block_mask(mod_stats* stats, const void* q, const void* k
                                   void* stream);
 
 /* Device workspace the attention call needs, in bytes (about
- * 4 * B * H * (n/2 + 11); 0 for an invalid shape).  It holds the call's work
+ * 4 * (B * H * (n/2 + 11) + 288); 0 for an invalid shape).  It holds the call's work
  * plan: the (head, pair of query blocks) items ordered and spread over the
  * chip by their list lengths.  Owned by the caller, rewritten by every call;
  * two calls in flight at once need two workspaces. */
@@ -208,7 +208,9 @@ size_t mod_attn_workspace_bytes(const mod_shape* shape);
  *   O_p = sum over tokens q of the kept blocks of softmax_q(scale * Q_p.K_q) V_q
  *   lse_p = log sum_q exp(scale * Q_p.K_q)        (natural log)
  * with the kept blocks kv_idx[row][0 .. kv_cnt[row]) (layout of
- * mod_predict_block_mask; indices in [0, n), each at most once).  A row with
+ * mod_predict_block_mask; indices in [0, n), each at most once).  kv_idx
+ * must be the whole [B, H, n, n] array: every slot of a row may be read
+ * (those at or past kv_cnt are loaded with the row and ignored).  A row with
  * kv_cnt = 0 gives O = 0 and lse = -inf.  scale = 0 means 1/sqrt(d).
  * q, k, v, o: [B,H,L,d] bf16 device; lse: [B,H,L] fp32 device or NULL.
  * bf16 MFMA products, fp32 softmax and accumulation.  `frame_tokens` and

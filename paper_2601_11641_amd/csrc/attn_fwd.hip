@@ -227,7 +227,8 @@ __device__ __forceinline__ void wait_vmcnt() {
 // ---------------------------------------------------------------------------
 constexpr int kPlanThreads = 256;
 constexpr int kPlanMaxHeads = 4096;
-constexpr int kPlanHdr = 32;          // ints: ctr[8], len[8], start[8], pad
+constexpr int kCtrStride = 32;        // ints between fetch counters (one 128-byte line each)
+constexpr int kPlanHdr = 8 * kCtrStride + 32;   // ints: ctr[8] (strided), len[8], start[8], pad
 constexpr int kPlanSortMax = 8192;    // longer XCD lists keep the head order
 constexpr int kPlanBuckets = 512;
 
@@ -242,8 +243,8 @@ struct Plan {
     __host__ __device__ Plan(void* ws, int BH) {
         int* w = static_cast<int*>(ws);
         ctr = w;
-        len = w + 8;
-        start = w + 16;
+        len = w + 8 * kCtrStride;
+        start = len + 8;
         tot = w + kPlanHdr;
         order = tot + BH;
         bounds = order + BH;
@@ -369,7 +370,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_lists_kernel(const int32_t*
     if (t == 0) {
         pl.len[x] = xtot[x];
         pl.start[x] = first;
-        pl.ctr[x] = 0;
+        pl.ctr[kCtrStride * x] = 0;
     }
     // Longest items first: a bucket sort of the list by decreasing cost
     // (order within a bucket unspecified; the order only affects timing).
@@ -419,7 +420,7 @@ __device__ __forceinline__ int fetch_item(const Plan& pl, int x) {
         const int xx = (x + a) % kXcds;
         const int len = pl.len[xx];
         if (len == 0) continue;
-        const int k = atomicAdd(&pl.ctr[xx], 1);
+        const int k = atomicAdd(&pl.ctr[kCtrStride * xx], 1);
         if (k < len) return pl.items[pl.start[xx] + k];
     }
     return -1;
@@ -432,20 +433,34 @@ __device__ __forceinline__ int fetch_item(const Plan& pl, int x) {
 template <int NT>
 __device__ __forceinline__ void mark_rows(const int32_t* __restrict__ kv_idx, const int32_t* __restrict__ kv_cnt,
                                           size_t row0, bool has1, int n, uint8_t* umask, int tid) {
-    const int cnt0 = min(max(kv_cnt[row0], 0), n);
-    const int cnt1 = has1 ? min(max(kv_cnt[row0 + 1], 0), n) : 0;
+    // the counts and every entry slot of both rows are loaded at once (one
+    // memory latency); slot a of a row is used only if a < its count
+    constexpr int EPT = kMaxBlocks / NT;
     const int32_t* list0 = kv_idx + row0 * n;
     const int32_t* list1 = list0 + n;
+    const int c0 = kv_cnt[row0];
+    const int c1 = has1 ? kv_cnt[row0 + 1] : 0;
+    int e0[EPT], e1[EPT];
+#pragma unroll
+    for (int x = 0; x < EPT; ++x) {
+        const int a = tid + x * NT;
+        e0[x] = a < n ? list0[a] : -1;
+        e1[x] = (has1 && a < n) ? list1[a] : -1;
+    }
+    const int cnt0 = min(max(c0, 0), n);
+    const int cnt1 = min(max(c1, 0), n);
     for (int j = tid; j < n; j += NT) umask[j] = 0;
     __syncthreads();
-    for (int a = tid; a < cnt0; a += NT) {
-        const int j = list0[a];
-        if ((unsigned)j < (unsigned)n) umask[j] = 1;
+#pragma unroll
+    for (int x = 0; x < EPT; ++x) {
+        const int j = e0[x];
+        if (tid + x * NT < cnt0 && (unsigned)j < (unsigned)n) umask[j] = 1;
     }
     __syncthreads();
-    for (int a = tid; a < cnt1; a += NT) {
-        const int j = list1[a];
-        if ((unsigned)j < (unsigned)n) umask[j] |= 2;
+#pragma unroll
+    for (int x = 0; x < EPT; ++x) {
+        const int j = e1[x];
+        if (tid + x * NT < cnt1 && (unsigned)j < (unsigned)n) umask[j] |= 2;
     }
     __syncthreads();
 }
@@ -628,10 +643,6 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
             val = *reinterpret_cast<const uint4*>(q + base + (size_t)qrow * D + 16 * kk + 8 * h);
         qreg[kk] = __builtin_bit_cast(bf16x8, val);
     }
-    // Q is complete before the tile loop: no wait on the memory counter
-    // (which also counts the tile copies) is left for the loop to inherit.
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) asm volatile("" : "+v"(qreg[kk]));
 
     f32x16 oacc[DT];
 #pragma unroll
@@ -833,6 +844,11 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     e_cur = __builtin_amdgcn_readfirstlane(e_cur);
     e_nxt = __builtin_amdgcn_readfirstlane(e_nxt);
     if (ns > 0) copy.issue_all(g == 0 ? kg : vg, (int)(e_cur & 0xFFFF), L, g == 0 ? kb0 : vb0, qw, lane);
+    // Q and the first tile are complete before the tile loop: no wait on
+    // the memory counter (which also counts the tile copies) is left for the
+    // loop to inherit.
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) asm volatile("" : "+v"(qreg[kk]));
     wait_copies();
     barrier();
     if (g == 1) barrier();   // group 1 starts one phase late
