@@ -436,7 +436,8 @@ __global__ __launch_bounds__(kThreads) void extrapolate_kernel(const double* __r
 }
 
 // ---------------------------------------------------------------------------
-// a5: per-row selection.  One workgroup per (head, query block i).
+// a5: per-row selection.  One wave per (head, query block i) up to n = 1024
+// (select_wave_kernel), one work-group of 256 threads per row above.
 //   sigma_j = n (c~[j-i] + d~[j]) in fp64, rounded to float: the ranking key.
 //   Non-forced blocks get the 64-bit key (order(sigma) << 32 | ~j), so one
 //   descending bitonic sort orders them by (sigma desc, j asc); forced blocks
@@ -460,9 +461,30 @@ __device__ inline float order_bits_to_float(uint32_t k) {
     return __uint_as_float(u);
 }
 
+// x of lane l ^ mask.  Masks 1 and 2 stay within a quad and 8 within a
+// row of 16 lanes (a rotation by 8), so they move through the DPP network
+// at no memory-pipeline cost; 32 swaps the wave's halves
+// (v_permlane32_swap with x in both operands returns x[l mod 32] and
+// x[l mod 32 + 32] to lane l); other masks use the LDS crossbar.
+template <bool kDpp>
+__device__ inline uint32_t xchg_u32(uint32_t x, int mask) {
+    if (!kDpp) return (uint32_t)__shfl_xor((int)x, mask);
+    switch (mask) {
+        case 1: return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, false);   // quad_perm 1,0,3,2
+        case 2: return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x4E, 0xF, 0xF, false);   // quad_perm 2,3,0,1
+        case 8: return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x128, 0xF, 0xF, false);  // row_ror:8
+        case 32: {
+            const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+            return (threadIdx.x & 32) ? r[0] : r[1];
+        }
+        default: return (uint32_t)__shfl_xor((int)x, mask);
+    }
+}
+
+template <bool kDpp>
 __device__ inline uint64_t shfl_xor_u64(uint64_t v, int mask) {
-    const uint32_t lo = __shfl_xor(static_cast<uint32_t>(v), mask);
-    const uint32_t hi = __shfl_xor(static_cast<uint32_t>(v >> 32), mask);
+    const uint32_t lo = xchg_u32<kDpp>(static_cast<uint32_t>(v), mask);
+    const uint32_t hi = xchg_u32<kDpp>(static_cast<uint32_t>(v >> 32), mask);
     return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
@@ -545,7 +567,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
                 uint64_t pv[E];
                 if (jj < 64 * E) {
 #pragma unroll
-                    for (int e = 0; e < E; ++e) pv[e] = shfl_xor_u64(kr[e], jj / E);
+                    for (int e = 0; e < E; ++e) pv[e] = shfl_xor_u64<(E <= 8)>(kr[e], jj / E);
                 } else {
                     __syncthreads();     // the previous exchange has been read
 #pragma unroll
@@ -626,6 +648,198 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     // text blocks after the video blocks: kept in every row
     for (int j = n + t; j < ldn; j += kThreads) out[total + (j - n)] = j;
     if (t == 0) kv_cnt[orow] = total + (ldn - n);
+}
+
+
+// The same selection with one wave per row (n <= 64 * EW): the row's keys in
+// registers, EW per lane (lane l holds positions EW*l .. EW*l+EW-1), every
+// stage of the sort, the forced-mass sum, the mass prefix, the choice of
+// the kept count and the compaction across the wave's lanes, so no
+// work-group barrier is needed; a wave's flags live in its own LDS bytes.
+// Four waves (rows) per work-group.
+__device__ inline double wave_sum_f64(double v) {
+    // butterfly: partners add the same two values, so every lane ends with
+    // the same bits (a fixed order)
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
+__device__ inline int wave_min_i32(int v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v = min(v, __shfl_xor(v, off));
+    return v;
+}
+
+template <class T>
+__device__ inline T wave_inclusive_scan(T v, int lane) {
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const T y = __shfl_up(v, off);
+        if (lane >= off) v += y;
+    }
+    return v;
+}
+
+__device__ inline void wave_sync_lds() {
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+}
+
+// Stage (KK, JJ) of a descending bitonic sort over the 64*EW keys of a wave
+// (lane l holds positions EW*l .. EW*l+EW-1): positions a and a ^ JJ are
+// compared, the lower one keeps the larger key when (a & KK) == 0.  The
+// stages are template arguments so that every exchange is resolved at
+// compile time (an unrolled loop over them exceeds the unroller's budget).
+template <int EW, int KK, int JJ>
+__device__ __forceinline__ void bitonic_stage_wave(uint64_t (&kr)[EW], int lane) {
+    if constexpr (JJ < EW) {
+#pragma unroll
+        for (int e = 0; e < EW; ++e) {
+            const int eb = e ^ JJ;
+            if (eb > e) {
+                const int a = EW * lane + e;
+                const bool desc = (a & KK) == 0;
+                const uint64_t ka = kr[e], kb = kr[eb];
+                const bool swap = desc ? (ka < kb) : (ka > kb);
+                kr[e] = swap ? kb : ka;
+                kr[eb] = swap ? ka : kb;
+            }
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < EW; ++e) {
+            const uint64_t pv = shfl_xor_u64<true>(kr[e], JJ / EW);
+            const int a = EW * lane + e;
+            const bool lower = (a & JJ) == 0;
+            const bool desc = (a & KK) == 0;
+            const uint64_t hi = kr[e] > pv ? kr[e] : pv;
+            const uint64_t lo = kr[e] > pv ? pv : kr[e];
+            kr[e] = (lower == desc) ? hi : lo;
+        }
+    }
+}
+
+template <int EW, int KK, int JJ>
+__device__ __forceinline__ void bitonic_merge_wave(uint64_t (&kr)[EW], int lane) {
+    bitonic_stage_wave<EW, KK, JJ>(kr, lane);
+    if constexpr (JJ > 1) bitonic_merge_wave<EW, KK, JJ / 2>(kr, lane);
+}
+
+template <int EW, int KK>
+__device__ __forceinline__ void bitonic_sort_wave(uint64_t (&kr)[EW], int lane) {
+    bitonic_merge_wave<EW, KK, KK / 2>(kr, lane);
+    if constexpr (KK < 64 * EW) bitonic_sort_wave<EW, 2 * KK>(kr, lane);
+}
+
+template <int EW>
+__global__ __launch_bounds__(kThreads) void select_wave_kernel(
+    const double* __restrict__ pred, const int32_t* __restrict__ gate,
+    const int* __restrict__ row_lo, const int* __restrict__ row_hi, int mode, int topk,
+    double tau, int32_t* __restrict__ kv_idx, int32_t* __restrict__ kv_cnt, int n,
+    int ldn, int tb0, int rows) {
+    constexpr int npad = 64 * EW;
+    constexpr int WPG = kThreads / 64;
+    __shared__ uint8_t flags[WPG][npad];
+    const int lane = threadIdx.x & 63;
+    const int wv = threadIdx.x >> 6;
+    const int row = blockIdx.x * WPG + wv;        // wave-uniform
+    if (row >= rows) return;
+    uint8_t* flag = flags[wv];
+
+    const int bh = row / n, i = row % n;
+    const double* c = pred + (size_t)bh * (3 * n - 1);
+    const double* d = c + (2 * n - 1);
+    const bool g = gate[bh] != 0;
+    const int flo = row_lo[i], fhi = row_hi[i];
+    const bool tb_in_frames = g && tb0 >= flo && tb0 <= fhi;
+    const int nf = (g ? (fhi - flo + 1) : 0) + ((tb0 < n && !tb_in_frames) ? 1 : 0);
+    const int n_free = n - nf;
+
+    double forced_mass = 0.0;
+    uint64_t kr[EW];
+#pragma unroll
+    for (int e = 0; e < EW; ++e) {
+        const int j = EW * lane + e;
+        uint64_t key = 0;
+        uint8_t fl = 0;
+        if (j < n) {
+            const double sv = static_cast<double>(n) * (c[j - i + n - 1] + d[j]);
+            const float kf = static_cast<float>(sv);
+            if ((g && j >= flo && j <= fhi) || j == tb0) {
+                fl = 1;
+                forced_mass += fmax(static_cast<double>(kf), 0.0);
+            } else {
+                key = (static_cast<uint64_t>(order_bits(kf)) << 32) |
+                      static_cast<uint64_t>(0xFFFFFFFFu - static_cast<uint32_t>(j));
+            }
+        }
+        kr[e] = key;
+        flag[j] = fl;
+    }
+
+    // descending bitonic sort of the npad keys (stages as in select_kernel;
+    // partners in other lanes are exchanged across the wave)
+    bitonic_sort_wave<EW, 2>(kr, lane);
+
+    int keep;
+    if (mode == 0) {
+        keep = min(n_free, max(0, topk - nf));
+    } else {
+        const double fm = wave_sum_f64(forced_mass);
+        // inclusive prefix of the positive masses in sorted order: within the
+        // lane, then the lanes' totals scanned across the wave
+        double part[EW];
+        double run = 0.0;
+#pragma unroll
+        for (int e = 0; e < EW; ++e) {
+            const int pos = EW * lane + e;
+            const double v =
+                pos < n_free
+                    ? fmax(static_cast<double>(order_bits_to_float(static_cast<uint32_t>(kr[e] >> 32))), 0.0)
+                    : 0.0;
+            run += v;
+            part[e] = run;
+        }
+        const double incl = wave_inclusive_scan(run, lane);
+        const double base = incl - run;                 // positions before this lane
+        const double all = __shfl(incl, 63);
+        const double target = tau * (fm + all);
+        const int kmin = nf > 0 ? 0 : 1;
+        // keeping `cand` free blocks reaches fm + (mass of positions < cand)
+        int best = n_free;
+#pragma unroll
+        for (int e = EW - 1; e >= 0; --e) {
+            const int cand = EW * lane + e;
+            if (cand < kmin || cand > n_free) continue;
+            const double before = cand == 0 ? 0.0 : (e == 0 ? base : base + part[e - 1]);
+            if (fm + before >= target) best = cand;
+        }
+        keep = wave_min_i32(best);
+    }
+    wave_sync_lds();
+#pragma unroll
+    for (int e = 0; e < EW; ++e) {
+        if (EW * lane + e < keep) flag[0xFFFFFFFFu - static_cast<uint32_t>(kr[e] & 0xFFFFFFFFull)] = 1;
+    }
+    wave_sync_lds();
+
+    // compaction in ascending j
+    int cnt = 0;
+#pragma unroll
+    for (int e = 0; e < EW; ++e) cnt += flag[EW * lane + e];
+    const int incl_c = wave_inclusive_scan(cnt, lane);
+    int pos = incl_c - cnt;
+    const int total = __shfl(incl_c, 63);
+    const size_t orow = (size_t)bh * ldn + i;     // row of the [BH, ldn, ldn] lists
+    int32_t* out = kv_idx + orow * ldn;
+#pragma unroll
+    for (int e = 0; e < EW; ++e) {
+        const int j = EW * lane + e;
+        if (flag[j]) out[pos++] = j;
+    }
+    for (int j = n + lane; j < ldn; j += 64) out[total + (j - n)] = j;
+    if (lane == 0) kv_cnt[orow] = total + (ldn - n);
 }
 
 inline unsigned cdiv(long a, long b) { return static_cast<unsigned>((a + b - 1) / b); }
@@ -821,6 +1035,26 @@ hipError_t launch_text_rows(int32_t* kv_idx, int32_t* kv_cnt, int BH, int ldn, i
 hipError_t launch_select(const double* pred, const int32_t* gate, const int* row_lo,
                          const int* row_hi, int mode, int k, double tau, int32_t* kv_idx,
                          int32_t* kv_cnt, int BH, int n, int ldn, int tb0, hipStream_t s) {
+    int npad_w = 64;
+    while (npad_w < n) npad_w <<= 1;
+    if (npad_w <= 1024) {   // one wave per row
+        const int rows = BH * n;
+        auto gow = [&](auto kern) {
+            hipLaunchKernelGGL(kern, dim3(cdiv(rows, kThreads / 64)), dim3(kThreads), 0, s, pred, gate, row_lo,
+                               row_hi, mode, k, tau, kv_idx, kv_cnt, n, ldn, tb0, rows);
+            return hipGetLastError();
+        };
+        hipError_t e;
+        switch (npad_w / 64) {
+            case 1: e = gow(select_wave_kernel<1>); break;
+            case 2: e = gow(select_wave_kernel<2>); break;
+            case 4: e = gow(select_wave_kernel<4>); break;
+            case 8: e = gow(select_wave_kernel<8>); break;
+            default: e = gow(select_wave_kernel<16>); break;
+        }
+        if (e != hipSuccess) return e;
+        return launch_text_rows(kv_idx, kv_cnt, BH, ldn, tb0, s);
+    }
     int npad = kThreads;
     while (npad < n) npad <<= 1;
     const size_t lds = (size_t)npad * (sizeof(uint64_t) + sizeof(double) + sizeof(int));
