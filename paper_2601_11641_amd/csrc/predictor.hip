@@ -519,10 +519,12 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     const int t = threadIdx.x;
 
     double forced_mass = 0.0;
-    uint64_t kr[E];                  // this thread's keys (positions E*t + e)
+    // thread t starts with the keys of blocks t + 256 e (coalesced loads) at
+    // positions E*t + e; the sort is indifferent to the starting placement
+    uint64_t kr[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-        const int j = E * t + e;
+        const int j = t + kThreads * e;   // coalesced; the sort places keys by value
         uint64_t key = 0;
         int fl = 0;
         if (j < n) {
@@ -652,7 +654,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
 
 
 // The same selection with one wave per row (n <= 64 * EW): the row's keys in
-// registers, EW per lane (lane l holds positions EW*l .. EW*l+EW-1), every
+// registers, EW per lane (lane l holds positions EW*l .. EW*l+EW-1 of the
+// sort, starting with the keys of blocks l + 64 e: coalesced loads), every
 // stage of the sort, the forced-mass sum, the mass prefix, the choice of
 // the kept count and the compaction across the wave's lanes, so no
 // work-group barrier is needed; a wave's flags live in its own LDS bytes.
@@ -760,7 +763,7 @@ __global__ __launch_bounds__(kThreads) void select_wave_kernel(
     uint64_t kr[EW];
 #pragma unroll
     for (int e = 0; e < EW; ++e) {
-        const int j = EW * lane + e;
+        const int j = lane + 64 * e;   // coalesced; the sort places keys by value
         uint64_t key = 0;
         uint8_t fl = 0;
         if (j < n) {
