@@ -224,6 +224,8 @@ __device__ __forceinline__ void wait_vmcnt() {
 // The attention work-groups are persistent (one per CU): a work-group
 // fetches the next item of its XCD's list with an atomic counter and, once
 // that list is drained, of the other XCDs' lists, until all are drained.
+// Each counter has a 128-byte line of its own, so the XCDs' atomics do not
+// queue on one line.
 // ---------------------------------------------------------------------------
 constexpr int kPlanThreads = 256;
 constexpr int kPlanMaxHeads = 4096;
@@ -233,7 +235,7 @@ constexpr int kPlanSortMax = 8192;    // longer XCD lists keep the head order
 constexpr int kPlanBuckets = 512;
 
 struct Plan {
-    int* ctr;       // [8] fetch counters
+    int* ctr;       // fetch counters, ctr[kCtrStride * x] for XCD x
     int* len;       // [8] items per XCD list
     int* start;     // [8] first item of each XCD list in `items`
     int* tot;       // [BH] total cost per head
