@@ -255,7 +255,11 @@ def reconstruct(X: np.ndarray, n: int, regions) -> np.ndarray:
 
 
 def nae(G: np.ndarray, X: np.ndarray, regions) -> float:
-    """Normalised approximation error ||R|| / ||S|| (Section 4.2), diagnostic."""
+    """Normalised approximation error ||R|| / ||S|| (Section 4.2) of the fit X
+    to the statistic G, R = G - M X.  Reading: the norm is the 2-norm of the
+    vectorised map (Eq. 4 fits vec(S)), i.e. the Frobenius norm.  Diagnostic.
+    Pinned by a planted fit (NAE 0) and by a planted fit plus a residual
+    orthogonal to the model space (NAE = |residual| / |G|)."""
     R = G - reconstruct(X, G.shape[0], regions)
     return float(np.linalg.norm(R) / np.linalg.norm(G))
 
@@ -268,9 +272,11 @@ def nae(G: np.ndarray, X: np.ndarray, regions) -> float:
 def extrapolate(X1: np.ndarray | None, t1: int | None, X2: np.ndarray, t2: int, t: int, n: int):
     """Predicted (c~, d~) at step t from anchors (t1, X1), (t2, X2), t1 < t2
     (Section 5.2): x~ = x2 + (x2 - x1) / (t2 - t1) * (t - t2).  With a single
-    anchor the slope is taken as zero.  e is not extrapolated (Section 5.3
-    uses it only through the warm-up gate).  Pinned by exact reproduction of
-    linear sequences.
+    anchor the slope is taken as zero (the paper is silent; reading).  e is
+    not extrapolated (Section 5.3 uses it only through the warm-up gate).
+    Pinned by exact reproduction of linear sequences; the one-anchor branch
+    by the constant sequence (two equal anchors give the same prediction at
+    every step).
     """
     c2, d2, _ = split_coeffs(X2, n)
     if X1 is None:
@@ -759,13 +765,17 @@ def kept_block_flops(kept_lists, L: int, bs: int, d: int) -> float:
     return 4.0 * d * tot
 
 
-def exact_block_mass(q: np.ndarray, k: np.ndarray, bs: int, scale: float) -> np.ndarray:
+def exact_block_mass(q: np.ndarray, k: np.ndarray, bs: int, scale: float, rows=None) -> np.ndarray:
     """W(i, j) = (1/|i|) sum_{p in i} sum_{q in j} P(p, q) from the dense
-    attention probabilities of one head (diagnostic)."""
+    attention probabilities P of one head (Eq. 1 without a mask): the share
+    of query block i's attention that lands in key block j (diagnostic; rows
+    sum to 1).  rows: optional subset of query blocks (the others stay NaN).
+    Pinned by a library softmax brute force on a ragged shape and by the
+    uniform-attention closed form W(i, j) = |j| / L."""
     L = q.shape[0]
     n = num_blocks(L, bs)
-    W = np.zeros((n, n))
-    for i in range(n):
+    W = np.full((n, n), np.nan)
+    for i in (range(n) if rows is None else rows):
         qs = slice(i * bs, min(L, (i + 1) * bs))
         a = scale * (q[qs] @ k.T)
         P = np.exp(a - a.max(axis=1, keepdims=True))
@@ -775,9 +785,46 @@ def exact_block_mass(q: np.ndarray, k: np.ndarray, bs: int, scale: float) -> np.
     return W
 
 
+def block_energy(q: np.ndarray, k: np.ndarray, bs: int, scale: float, rows=None) -> np.ndarray:
+    """E(i, j) = sum_{p in i} sum_{q in j} P(p, q)^2 over the dense attention
+    probabilities P of one head: the squared Frobenius norm of block (i, j)
+    of the attention map, from which the SMFS of a block mask follows
+    (diagnostic).  rows: optional subset of query blocks (others NaN).
+    Pinned with smfs()."""
+    L = q.shape[0]
+    n = num_blocks(L, bs)
+    E = np.full((n, n), np.nan)
+    for i in (range(n) if rows is None else rows):
+        qs = slice(i * bs, min(L, (i + 1) * bs))
+        a = scale * (q[qs] @ k.T)
+        P = np.exp(a - a.max(axis=1, keepdims=True))
+        P /= P.sum(axis=1, keepdims=True)
+        for j in range(n):
+            blk = P[:, j * bs:min(L, (j + 1) * bs)]
+            E[i, j] = (blk * blk).sum()
+    return E
+
+
+def smfs(E: np.ndarray, kept_lists, rows=None) -> float:
+    """Sparsity Mask Fidelity Score (the paper's SMFS appendix):
+    ||A . M||_F / ||A||_F for the dense attention map A and the token mask M
+    of the block lists, from the block energies E of block_energy() (over
+    the query blocks ``rows``, default all).  The paper calls a lower score
+    better although the ratio measures the retained norm; it is reported as
+    defined (reading: higher = more of the map retained).  Pinned by a
+    token-level brute force with the upsampled mask and by the uniform
+    closed form sqrt(kept tokens) / L."""
+    rr = range(E.shape[0]) if rows is None else rows
+    kept = sum(E[i, np.asarray(kept_lists[i], dtype=np.int64)].sum() for i in rr)
+    total = sum(E[i].sum() for i in rr)
+    return float(math.sqrt(kept / total))
+
+
 def sparsity_map(q: np.ndarray, k: np.ndarray, bs: int, scale: float, eta: float) -> np.ndarray:
     """Eq. 2: fraction of attention probabilities below eta in each block
-    (probabilities read as the softmax output, as in Algorithm 1).  Diagnostic."""
+    (probabilities read as the softmax output, as in Algorithm 1).  Diagnostic.
+    Pinned by the per-entry library softmax brute force of the statistic
+    (its complement on full lists) and the uniform-attention closed form."""
     L = q.shape[0]
     n = num_blocks(L, bs)
     S = np.zeros((n, n))
@@ -792,7 +839,9 @@ def sparsity_map(q: np.ndarray, k: np.ndarray, bs: int, scale: float, eta: float
     return S
 
 
-def mask_recall(W: np.ndarray, kept_lists) -> float:
-    """Mean over query blocks of the dense attention mass the mask keeps."""
-    return float(np.mean([W[i, np.asarray(js, dtype=np.int64)].sum()
-                          for i, js in enumerate(kept_lists)]))
+def mask_recall(W: np.ndarray, kept_lists, rows=None) -> float:
+    """Mean over query blocks (``rows``, default all) of the dense attention
+    mass the mask keeps: sum over kept j of W(i, j) (diagnostic).  Pinned by
+    hand-computed values and the full-mask value 1."""
+    rr = range(W.shape[0]) if rows is None else rows
+    return float(np.mean([W[i, np.asarray(kept_lists[i], dtype=np.int64)].sum() for i in rr]))

@@ -39,18 +39,86 @@ def gpu_lists(kv_idx, kv_cnt) -> list:
 
 
 def row_invariants_ok(row: list, n: int, forced: np.ndarray, mode: str, k: int,
-                      sig_row: np.ndarray, tau: float) -> bool:
-    """What any correct selection of the row satisfies, whatever the tie order."""
-    if row != sorted(set(row)) or (row and (row[0] < 0 or row[-1] >= n)) or not row:
+                      sig_row: np.ndarray, tau: float, tol: float = GAP) -> bool:
+    """What any correct selection of the row satisfies, whatever the order of
+    keys within ``tol`` of each other (Section 5.3 with the per-row reading):
+
+    * sorted, unique, in [0, n), non-empty, a superset of the forced blocks;
+    * ordering: among the non-forced blocks no dropped block's float32 key
+      exceeds a kept one's by more than ``tol``;
+    * TOPK: exactly max(k, |forced|) blocks (capped at n);
+    * MASS: the kept positive key mass reaches tau of the row's total
+      (reach), and dropping the lowest-keyed non-forced kept block falls
+      below it (minimality), unless that block is the one a row without
+      forced blocks must keep.
+    """
+    if not row or row != sorted(set(row)) or row[0] < 0 or row[-1] >= n:
         return False
     fset = set(np.flatnonzero(forced).tolist())
-    if not fset.issubset(row):
+    rset = set(row)
+    if not fset.issubset(rset):
         return False
-    free = n - len(fset)
+    keys = sig_row.astype(np.float32).astype(np.float64)
+    kept_free = [j for j in row if j not in fset]
+    dropped = [j for j in range(n) if j not in rset and j not in fset]
+    if kept_free and dropped and keys[kept_free].min() < keys[dropped].max() - tol:
+        return False
     if mode == "topk":
+        free = n - len(fset)
         return len(row) == len(fset) + min(free, max(0, k - len(fset)))
-    keys = np.maximum(sig_row.astype(np.float32).astype(np.float64), 0.0)
-    return keys[row].sum() >= np.float32(tau) * keys.sum() - 1e-9 * max(1.0, keys.sum())
+    pos = np.maximum(keys, 0.0)
+    total = math.fsum(pos)
+    target = float(np.float32(tau)) * total
+    slack = 1e-12 * total               # summation-order rounding of the two sides
+    kept_mass = math.fsum(pos[row])
+    if kept_mass < target - slack:
+        return False
+    kmin = 0 if fset else 1
+    if len(kept_free) > kmin:
+        last = min(kept_free, key=lambda j: (keys[j], -j))   # the last block of the order
+        if kept_mass - pos[last] >= target + slack:
+            return False
+    return True
+
+
+def pattern_head_ok(gpu_rows: list, ctil: np.ndarray, dtil: np.ndarray, n: int, K: int,
+                    forced: np.ndarray, tol: float) -> bool:
+    """Validity of a head's pattern-mode mask when keys tie within ``tol``:
+    the K chosen patterns must contain every pattern whose float32 key is
+    above the band [kth - tol, kth + tol] around the K-th key and none below
+    it, so the mask must be (sure patterns) + forced + some band patterns,
+    each chosen band pattern fully kept, with room for them in K."""
+    vals = np.concatenate([ctil, dtil]).astype(np.float32).astype(np.float64)
+    P = vals.size
+    order = np.lexsort((np.arange(P), -vals))
+    kth = vals[order[min(K, P) - 1]]
+    sure = vals > kth + tol
+    band = (np.abs(vals - kth) <= tol)
+    i, j = np.indices((n, n))
+    dg = j - i + n - 1
+    col = 2 * n - 1 + j
+
+    def cover(sel):
+        return sel[dg] | sel[col]
+
+    mask = np.zeros((n, n), bool)
+    for r, js in enumerate(gpu_rows):
+        if js != sorted(set(js)) or (js and (js[0] < 0 or js[-1] >= n)):
+            return False
+        mask[r, js] = True
+    base = cover(sure) | forced
+    if (base & ~mask).any():
+        return False
+    # band patterns whose every block is kept are the only ones that can be chosen
+    full_band = np.zeros(P, bool)
+    for pidx in np.flatnonzero(band):
+        cells = (dg == pidx) if pidx < 2 * n - 1 else (col == pidx)
+        full_band[pidx] = bool(mask[cells].all())
+    explained = base | cover(full_band)
+    if (mask & ~explained).any():
+        return False
+    need = K - int(sure.sum())
+    return 0 <= need <= int(full_band.sum())
 
 
 def compare_lists(gpu_rows: list, oracle_rows: list, sig: np.ndarray, forced: np.ndarray,
@@ -74,14 +142,19 @@ def compare_lists(gpu_rows: list, oracle_rows: list, sig: np.ndarray, forced: np
     return nrows, exact, excused, bad
 
 
-def compare_pattern_head(gpu_rows: list, oracle_rows: list, n: int):
+def compare_pattern_head(gpu_rows: list, oracle_rows: list, n: int, ctil=None, dtil=None,
+                         K: int = 0, forced=None):
     """Pattern mode decides per head: the GPU lists must equal the oracle's
     unless the head's boundary key gap (scaled by n like the row scores) is
-    within GAP.  Returns (n_rows, n_exact, excused_head, mismatching rows)."""
+    within GAP, and then the GPU mask must be a valid choice of K patterns
+    under ties within GAP / n (pattern_head_ok; checked when the predicted
+    ctil, dtil are given).  Returns (n_rows, n_exact, excused_head,
+    mismatching rows)."""
     same = [i for i in range(n) if gpu_rows[i] == oracle_rows[i].kept.tolist()]
     if len(same) == n:
         return n, n, False, []
-    if n * oracle_rows[0].key_gap <= GAP:
+    if n * oracle_rows[0].key_gap <= GAP and (
+            ctil is None or pattern_head_ok(gpu_rows, ctil, dtil, n, K, forced, GAP / n)):
         return n, len(same), True, []
     return n, len(same), False, [i for i in range(n) if i not in set(same)]
 

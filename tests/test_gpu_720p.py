@@ -80,7 +80,9 @@ def _check_heads(cfg, host, st, idx, cnt, budget, heads):
         assert np.abs(X[0, h] - Xo[0, hi]).max() <= 1e-9 * max(1.0, np.abs(Xo[0, hi]).max())
         assert bool(gate[0, h]) == bool(P.gates[0, hi])
         if mode == "pattern":
-            nr, _, xh, bad = compare_pattern_head(rows[0][h], sel[0][hi], n)
+            ct, dt_ = P.prediction(WARM + 1)[0][hi]
+            forced = O.forced_mask(n, P.regions, bool(P.gates[0, hi]))
+            nr, _, xh, bad = compare_pattern_head(rows[0][h], sel[0][hi], n, ct, dt_, val, forced)
             assert not bad, f"head {h}: rows {bad[:10]} differ"
             total, excused = total + nr, excused + (nr if xh else 0)
             continue

@@ -110,7 +110,9 @@ def _check_predictor(cfg, st, kv_idx, kv_cnt, P, sel, qf, kf, budget, step):
         heads_excused = 0
         for b in range(B):
             for h in range(H):
-                nr, ne, xh, bad = compare_pattern_head(rows[b][h], sel[b][h], n)
+                ct, dt_ = po[b][h]
+                forced = O.forced_mask(n, P.regions, bool(P.gates[b, h]))
+                nr, ne, xh, bad = compare_pattern_head(rows[b][h], sel[b][h], n, ct, dt_, val, forced)
                 assert not bad, f"head ({b},{h}) rows {bad[:10]} differ"
                 heads_excused += int(xh)
         assert heads_excused <= max(1, 0.05 * B * H), heads_excused

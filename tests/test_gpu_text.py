@@ -17,7 +17,7 @@ import pytest
 import oracle as O
 import workloads as W
 from parity import (GAP, LSE_ABS, MAX_ABS, MEAN_ABS, attention_errors, bf16_tensor, bf16_to_f64,
-                    compare_lists, gpu_lists)
+                    compare_lists, gpu_lists, pattern_head_ok)
 
 import paper_2601_11641_amd as M
 
@@ -84,6 +84,9 @@ def _check_text_head(P, g_rows, o_rows, ct, dt_, gate_on, budget):
         same = all(g_rows[i] == o_rows[i].kept.tolist() for i in range(nt))
         if not same:
             assert nv * o_rows[0].key_gap <= GAP, "pattern lists differ beyond the gap rule"
+            gv = [[j for j in g_rows[i] if j < nv] for i in range(nv)]
+            assert pattern_head_ok(gv, ct, dt_, nv, budget[1], P.forced(gate_on), GAP / nv), \
+                "excused pattern lists are not a valid choice of patterns"
             return nt, nt
         return nt, 0
     gv = [[j for j in g_rows[i] if j < nv] for i in range(nv)]

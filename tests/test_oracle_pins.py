@@ -629,3 +629,154 @@ def test_predictor_identical_steps_give_identical_masks():
     for h in range(2):
         for ra, rb in zip(a[0][h], b[0][h]):
             assert ra.kept.tolist() == rb.kept.tolist()
+
+
+# ---------------------------------------------- one-anchor extrapolation (a4)
+
+def test_extrapolation_one_anchor_is_the_constant_sequence():
+    """With one anchor the slope is zero (reading; the paper is silent): the
+    prediction is the anchor's c, d at every step, which is what the
+    two-anchor formula gives for a constant sequence (two equal anchors)."""
+    rng = np.random.default_rng(17)
+    n, F = 7, 3
+    X2 = rng.standard_normal(O.num_coeffs(n, F))
+    c2, d2, _ = O.split_coeffs(X2, n)
+    for t2, t in [(1, 2), (5, 6), (5, 50), (3, 3)]:
+        c, d = O.extrapolate(None, None, X2, t2, t, n)
+        assert np.array_equal(c, c2) and np.array_equal(d, d2)
+        cc, dd = O.extrapolate(X2.copy(), t2 - 1, X2, t2, t, n)
+        assert np.array_equal(c, cc) and np.array_equal(d, dd)
+    # the returned arrays are copies: the anchor is not changed through them
+    c, d = O.extrapolate(None, None, X2, 1, 2, n)
+    c += 1.0
+    assert np.array_equal(O.split_coeffs(X2, n)[0], c2)
+
+
+# ------------------------------------------------------- diagnostics (O10)
+
+def _ragged_head(seed, L=37, d=4):
+    rng = np.random.default_rng(seed)
+    return rng.standard_normal((L, d)), rng.standard_normal((L, d))
+
+
+def test_exact_block_mass_library_softmax_bruteforce():
+    """W(i, j) against scipy's softmax of every token row, summed by
+    explicit loops over the tokens of each block (ragged: 8, 8, 8, 8, 5)."""
+    q, k = _ragged_head(21)
+    L, bs, scale = 37, 8, 0.6
+    n = O.num_blocks(L, bs)
+    W = O.exact_block_mass(q, k, bs, scale)
+    for i in range(n):
+        toks = [p for p in range(L) if p // bs == i]
+        for j in range(n):
+            tot = 0.0
+            for p in toks:
+                pr = scipy.special.softmax(scale * (k @ q[p]))
+                tot += sum(pr[c] for c in range(L) if c // bs == j)
+            assert W[i, j] == pytest.approx(tot / len(toks), rel=1e-12, abs=1e-15)
+    np.testing.assert_allclose(W.sum(axis=1), 1.0, atol=1e-12)
+    sub = O.exact_block_mass(q, k, bs, scale, rows=[1, 4])
+    np.testing.assert_array_equal(sub[[1, 4]], W[[1, 4]])
+    assert np.isnan(sub[[0, 2, 3]]).all()
+
+
+def test_exact_block_mass_uniform_closed_form():
+    """q = 0: uniform attention, W(i, j) = |j| / L (the tail block's share is
+    its true size)."""
+    _, k = _ragged_head(22)
+    L, bs = 37, 8
+    W = O.exact_block_mass(np.zeros_like(k), k, bs, 1.0)
+    want = O.block_sizes(L, bs) / L
+    for i in range(W.shape[0]):
+        np.testing.assert_allclose(W[i], want, atol=1e-15)
+
+
+def test_smfs_token_level_bruteforce():
+    """SMFS = ||A . M||_F / ||A||_F with the block lists upsampled to a token
+    mask M and A from scipy's softmax, against block_energy + smfs."""
+    q, k = _ragged_head(23)
+    L, bs, scale = 37, 8, 0.8
+    n = O.num_blocks(L, bs)
+    rng = np.random.default_rng(24)
+    lists = [sorted(rng.choice(n, size=int(rng.integers(1, n + 1)), replace=False).tolist())
+             for _ in range(n)]
+    A = scipy.special.softmax(scale * (q @ k.T), axis=1)
+    Mtok = np.zeros((L, L))
+    for p in range(L):
+        for c in range(L):
+            if (c // bs) in lists[p // bs]:
+                Mtok[p, c] = 1.0
+    want = math.sqrt(((A * Mtok) ** 2).sum()) / math.sqrt((A ** 2).sum())
+    E = O.block_energy(q, k, bs, scale)
+    assert O.smfs(E, lists) == pytest.approx(want, rel=1e-12)
+    full = [list(range(n))] * n
+    assert O.smfs(E, full) == pytest.approx(1.0, rel=1e-14)
+    # a subset of query blocks: the same ratio over those token rows
+    rows = [0, 3]
+    sel = np.array([p // bs in rows for p in range(L)])
+    want_r = math.sqrt(((A * Mtok)[sel] ** 2).sum()) / math.sqrt((A[sel] ** 2).sum())
+    assert O.smfs(E, lists, rows=rows) == pytest.approx(want_r, rel=1e-12)
+
+
+def test_smfs_uniform_closed_form():
+    """q = 0: every probability of a row is 1/L, so ||A . M||^2 counts the
+    kept tokens / L^2 and ||A||^2 = 1: SMFS = sqrt(kept tokens) / L."""
+    _, k = _ragged_head(25)
+    L, bs = 37, 8
+    lists = [[0], [1, 4], [0, 2, 3], [4], [0, 1, 2, 3, 4]]
+    sizes = O.block_sizes(L, bs)
+    kept_tokens = sum(int(sizes[i]) * int(sizes[lists[i]].sum()) for i in range(5))
+    E = O.block_energy(np.zeros_like(k), k, bs, 1.0)
+    assert O.smfs(E, lists) == pytest.approx(math.sqrt(kept_tokens) / L, rel=1e-13)
+
+
+def test_mask_recall_hand_values():
+    W = np.array([[0.5, 0.3, 0.2],
+                  [0.1, 0.6, 0.3],
+                  [0.25, 0.25, 0.5]])
+    lists = [[0], [1, 2], [0, 2]]
+    # row sums kept: 0.5, 0.9, 0.75 -> mean 0.7166...
+    assert O.mask_recall(W, lists) == pytest.approx((0.5 + 0.9 + 0.75) / 3, abs=1e-15)
+    assert O.mask_recall(W, lists, rows=[1]) == pytest.approx(0.9, abs=1e-15)
+    assert O.mask_recall(W, [[0, 1, 2]] * 3) == pytest.approx(1.0, abs=1e-15)
+    assert O.mask_recall(W, [[], [], []]) == 0.0
+
+
+@pytest.mark.parametrize("L,bs,tf", [(256, 32, 64), (300, 32, 60)])
+def test_nae_planted_fit_and_orthogonal_residual(L, bs, tf):
+    """NAE(G, X) = ||G - M X|| / ||G||: 0 for a map the model reproduces
+    exactly; for a planted map plus a residual orthogonal to the model space
+    (projected out with the library least squares on the explicit M) the
+    fit recovers the planted part and NAE = ||residual|| / ||G||."""
+    n = O.num_blocks(L, bs)
+    reg = O.frame_regions(L, bs, tf)
+    rng = np.random.default_rng(26)
+    Msys = O.design_matrix(n, reg)
+    X0 = rng.standard_normal(Msys.shape[1])
+    G0 = (Msys @ X0).reshape(n, n)
+    assert O.nae(G0, O.fit(G0, reg), reg) < 1e-12
+    Rraw = rng.standard_normal(n * n)
+    Rperp = Rraw - Msys @ np.linalg.lstsq(Msys, Rraw, rcond=None)[0]
+    G = G0 + 0.3 * Rperp.reshape(n, n)
+    want = 0.3 * np.linalg.norm(Rperp) / np.linalg.norm(G)
+    assert O.nae(G, O.fit(G, reg), reg) == pytest.approx(want, rel=1e-9)
+    assert O.nae(G, X0, reg) == pytest.approx(want, rel=1e-9)
+
+
+def test_sparsity_map_library_softmax_bruteforce():
+    """Eq. 2 on the dense map: the fraction of scipy-softmax probabilities
+    below eta per block, counted entry by entry (ragged)."""
+    q, k = _ragged_head(27)
+    L, bs, scale, eta = 37, 8, 0.9, 0.02
+    n = O.num_blocks(L, bs)
+    S = O.sparsity_map(q, k, bs, scale, eta)
+    A = scipy.special.softmax(scale * (q @ k.T), axis=1)
+    sizes = O.block_sizes(L, bs)
+    for i in range(n):
+        for j in range(n):
+            below = sum(1 for p in range(L) for c in range(L)
+                        if p // bs == i and c // bs == j and A[p, c] < eta)
+            assert S[i, j] == below / (sizes[i] * sizes[j])
+    # uniform attention (q = 0): 1/L is below eta iff eta > 1/L
+    assert (O.sparsity_map(np.zeros_like(q), k, bs, 1.0, 1.0 / L * 1.01) == 1.0).all()
+    assert (O.sparsity_map(np.zeros_like(q), k, bs, 1.0, 1.0 / L * 0.99) == 0.0).all()
