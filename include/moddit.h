@@ -222,6 +222,26 @@ mod_status mod_block_sparse_attn_fwd(const mod_shape* shape, const void* q, cons
                                      const int32_t* kv_cnt, float scale, void* o, float* lse,
                                      void* workspace, size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory or pass a workspace (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): mod_block_sparse_attn_fwd with its work plan held in a
+ * library-owned device array of MOD_ATTN_NOALLOC_MAX_BYTES per device
+ * instead of a caller workspace.  Same arguments, layout, numerics and
+ * errors as mod_block_sparse_attn_fwd (its output is bit-identical);
+ * shapes whose workspace, mod_attn_workspace_bytes(shape), exceeds the
+ * array are rejected with MOD_ERR_UNSUPPORTED.  The call allocates nothing:
+ * the array is a static device variable whose address is resolved on the
+ * first call on each device (the current device, which must be the device
+ * of the pointers and the stream) and kept until the process ends.  Every
+ * call on a device shares that device's array, so calls that overlap on one
+ * device (concurrent streams, other threads) race on it and must be
+ * serialised by the caller; calls on one stream are ordered and safe. */
+#define MOD_ATTN_NOALLOC_MAX_BYTES (2u << 20)
+mod_status mod_block_sparse_attn_fwd_noalloc(const mod_shape* shape, const void* q, const void* k,
+                                             const void* v, const int32_t* kv_idx,
+                                             const int32_t* kv_cnt, float scale, void* o, float* lse,
+                                             void* stream);
+
 /* ---- introspection (synchronous copies to host memory; for tests) ---- */
 
 /* The sizes below count the nv video blocks (nv = n without text tokens). */

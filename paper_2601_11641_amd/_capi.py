@@ -75,6 +75,9 @@ _SIGS = {
     "mod_block_sparse_attn_fwd": (c_int, [POINTER(mod_shape), c_void_p, c_void_p, c_void_p,
                                           c_void_p, c_void_p, c_float, c_void_p, c_void_p,
                                           c_void_p, c_size_t, c_void_p]),
+    "mod_block_sparse_attn_fwd_noalloc": (c_int, [POINTER(mod_shape), c_void_p, c_void_p, c_void_p,
+                                                  c_void_p, c_void_p, c_float, c_void_p, c_void_p,
+                                                  c_void_p]),
     "mod_stats_get_anchor": (c_int, [c_void_p, c_int, POINTER(c_double), POINTER(c_int)]),
     "mod_stats_get_pooled": (c_int, [c_void_p, POINTER(c_double), POINTER(c_double)]),
     "mod_stats_get_block_mass": (c_int, [c_void_p, POINTER(c_double)]),
@@ -209,6 +212,20 @@ def mod_block_sparse_attn_fwd(shape: mod_shape, q, k, v, kv_idx, kv_cnt, scale: 
         _ptr(kv_cnt, "kv_cnt", "torch.int32"), float(scale), _ptr(o, "o", "torch.bfloat16"),
         _ptr(lse, "lse", "torch.float32"), _ptr(workspace, "workspace"), ws_bytes,
         _stream(stream)), "mod_block_sparse_attn_fwd")
+
+
+MOD_ATTN_NOALLOC_MAX_BYTES = 2 << 20
+
+
+def mod_block_sparse_attn_fwd_noalloc(shape: mod_shape, q, k, v, kv_idx, kv_cnt, scale: float, o,
+                                      lse=None, stream=None) -> None:
+    """The attention forward with its work plan in the library's own device
+    array (no workspace, no allocation in the library or here)."""
+    _check(_lib.mod_block_sparse_attn_fwd_noalloc(
+        ctypes.byref(shape), _ptr(q, "q", "torch.bfloat16"), _ptr(k, "k", "torch.bfloat16"),
+        _ptr(v, "v", "torch.bfloat16"), _ptr(kv_idx, "kv_idx", "torch.int32"),
+        _ptr(kv_cnt, "kv_cnt", "torch.int32"), float(scale), _ptr(o, "o", "torch.bfloat16"),
+        _ptr(lse, "lse", "torch.float32"), _stream(stream)), "mod_block_sparse_attn_fwd_noalloc")
 
 
 def _dbl(n):

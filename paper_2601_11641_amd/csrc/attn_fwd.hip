@@ -37,6 +37,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <mutex>
 #include <type_traits>
 
 namespace moddit {
@@ -1188,6 +1189,42 @@ hipError_t launch_count(const uint16_t* q, const uint16_t* k, const int32_t* kv_
 }
 
 }  // namespace
+
+// ---------------------------------------------------------------------------
+// Work plan in library-owned device memory, for callers that cannot
+// allocate: one array per device (each device holds its own copy at its
+// own address), kept until the process ends and shared by every call on
+// that device.  Host code never passes the array's name to a kernel (on the
+// host it only names a stand-in); the device address comes from
+// hipGetSymbolAddress, resolved once per device with that device current.
+// Nothing in it needs clearing between calls: the plan kernels rewrite every
+// field the attention reads (the fetch counters included) before it runs.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kScratchDevices] = {};
+}  // namespace
+
+hipError_t noalloc_scratch(void** out) {
+    *out = nullptr;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (ptr == nullptr) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
 
 size_t attn_workspace_bytes(int BH, int n) {
     const size_t ints = (size_t)kPlanHdr + (size_t)BH * (11 + (size_t)(n + 1) / 2);

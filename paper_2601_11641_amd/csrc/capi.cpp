@@ -522,6 +522,26 @@ mod_status mod_block_sparse_attn_fwd(const mod_shape* shape, const void* q, cons
     return MOD_OK;
 }
 
+mod_status mod_block_sparse_attn_fwd_noalloc(const mod_shape* shape, const void* q, const void* k,
+                                             const void* v, const int32_t* kv_idx,
+                                             const int32_t* kv_cnt, float scale, void* o, float* lse,
+                                             void* stream) {
+    mod_status st = check_shape(shape, false);
+    if (st != MOD_OK) return st;
+    const size_t need = moddit::attn_workspace_bytes(shape->B * shape->H, ceil_div(shape->L, shape->block));
+    if (need > (size_t)MOD_ATTN_NOALLOC_MAX_BYTES)
+        return fail(MOD_ERR_UNSUPPORTED,
+                    "work plan of %zu bytes exceeds the %zu-byte library array of the no-allocation "
+                    "entry point (B*H*(11 + ceil(n/2)) too large); use mod_block_sparse_attn_fwd",
+                    need, (size_t)MOD_ATTN_NOALLOC_MAX_BYTES);
+    static_assert(moddit::kNoAllocScratchBytes == (size_t)MOD_ATTN_NOALLOC_MAX_BYTES,
+                  "header and library disagree on the scratch size");
+    void* ws = nullptr;
+    const hipError_t e = moddit::noalloc_scratch(&ws);
+    if (e != hipSuccess) return hip_fail(e, "device address of the library work-plan array");
+    return mod_block_sparse_attn_fwd(shape, q, k, v, kv_idx, kv_cnt, scale, o, lse, ws, need, stream);
+}
+
 mod_status mod_stats_get_anchor(const mod_stats* s, int slot, double* host_coeffs, int* step) {
     if (!s || !host_coeffs) return fail(MOD_ERR_INVALID_ARG, "NULL argument");
     if (slot < 0 || slot > 1) return fail(MOD_ERR_INVALID_ARG, "slot must be 0 or 1");

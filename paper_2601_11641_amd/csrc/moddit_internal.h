@@ -63,6 +63,12 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
                            uint16_t* o, float* lse, int BH, int L, int d, int bs, int n,
                            void* ws, hipStream_t s);
 
+// The attention's work plan in a library-owned device array of
+// kNoAllocScratchBytes per device (for callers that cannot allocate):
+// the current device's address of that array, resolved on first use.
+constexpr size_t kNoAllocScratchBytes = size_t(2) << 20;
+hipError_t noalloc_scratch(void** out);
+
 // Eq. 2 statistic of a computed attention map: stat[bh][i][j] = fraction of
 // the probabilities of listed block (i, j) that reach exp(log_eta), with the
 // row LSE of the attention forward over the same lists; unlisted blocks keep
