@@ -681,7 +681,8 @@ class Predictor:
 
 
 def attention_statistic(q: np.ndarray, k: np.ndarray, kept_lists, bs: int, scale: float,
-                        eta: float, lse: np.ndarray | None = None, tol: float = 0.0, rows=None):
+                        eta: float, lse: np.ndarray | None = None, tol: float = 0.0, rows=None,
+                        return_lse: bool = False):
     """Eq. 2 on the attention map a step computed: for every kept block
     (i, j), the fraction of its probabilities A(p, q) = exp(scale q_p.k_q -
     LSE_p) that reach eta, where LSE_p normalises over the kept blocks of
@@ -695,12 +696,14 @@ def attention_statistic(q: np.ndarray, k: np.ndarray, kept_lists, bs: int, scale
     with NaN for blocks not kept; amb [n, n] the number of entries whose
     log-probability lies within tol of log(eta) (where two implementations
     may round the decision differently).  rows: optional subset of query
-    blocks (the other rows stay NaN / 0).
+    blocks (the other rows stay NaN / 0).  return_lse: also return the row
+    LSE used ([L], NaN outside ``rows``).
     """
     L = q.shape[0]
     n = num_blocks(L, bs)
     I = np.full((n, n), np.nan)
     amb = np.zeros((n, n), dtype=np.int64)
+    used = np.full(L, np.nan)
     log_eta = math.log(eta)
     for i in (range(n) if rows is None else rows):
         blocks = list(kept_lists[i])
@@ -714,6 +717,7 @@ def attention_statistic(q: np.ndarray, k: np.ndarray, kept_lists, bs: int, scale
             row_lse = mx + np.log(np.exp(a - mx).sum(axis=1, keepdims=True))
         else:
             row_lse = lse[qs][:, None]
+        used[qs] = row_lse[:, 0]
         logp = a - row_lse
         start = 0
         for j in blocks:
@@ -722,7 +726,7 @@ def attention_statistic(q: np.ndarray, k: np.ndarray, kept_lists, bs: int, scale
             start += w
             I[i, j] = float((blk >= log_eta).sum()) / blk.size
             amb[i, j] = int((np.abs(blk - log_eta) < tol).sum())
-    return I, amb
+    return (I, amb, used) if return_lse else (I, amb)
 
 
 def reconstruct_statistic(history: np.ndarray | None, current: np.ndarray) -> np.ndarray:

@@ -122,8 +122,13 @@ def pattern_head_ok(gpu_rows: list, ctil: np.ndarray, dtil: np.ndarray, n: int, 
 
 
 def compare_lists(gpu_rows: list, oracle_rows: list, sig: np.ndarray, forced: np.ndarray,
-                  mode: str, k: int = 0, tau: float = 1.0, rows=None):
-    """Returns (n_rows, n_exact, n_excused, mismatches) for one head."""
+                  mode: str, k: int = 0, tau: float = 1.0, rows=None, gap=None):
+    """Returns (n_rows, n_exact, n_excused, mismatches) for one head.
+
+    gap: the excuse threshold on the oracle's boundary key gap (and mass
+    margin), GAP by default; an array [n] gives one per row (rows whose
+    scores carry a known uncertainty).  It is also the ordering tolerance of
+    the invariants an excused row must satisfy."""
     n = sig.shape[0]
     exact = excused = 0
     bad = []
@@ -133,8 +138,9 @@ def compare_lists(gpu_rows: list, oracle_rows: list, sig: np.ndarray, forced: np
         if g == o.kept.tolist():
             exact += 1
             continue
-        if (o.key_gap <= GAP or o.mass_margin <= GAP) and \
-                row_invariants_ok(g, n, forced[i], mode, k, sig[i], tau):
+        gi = GAP if gap is None else float(np.broadcast_to(gap, (n,))[i])
+        if (o.key_gap <= gi or o.mass_margin <= gi) and \
+                row_invariants_ok(g, n, forced[i], mode, k, sig[i], tau, tol=gi):
             excused += 1
             continue
         bad.append(i)

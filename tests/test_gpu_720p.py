@@ -119,15 +119,54 @@ def _check_attention_rows(cfg, host, dev, idx, cnt, heads, nrows=5):
             assert np.abs(lg[sl] - Lo[sl]).max() <= LSE_ABS
 
 
-def test_720p_mass_budget(layer):
-    """The benchmark's budget (cumulative mass 0.75) on the whole layer."""
+@pytest.fixture(scope="module")
+def mass_run(layer):
+    """The benchmark's budget (cumulative mass 0.75) predicted and attended
+    on the whole layer, as the benchmark launches it; the lists and the
+    outputs of the sampled heads are kept on the host."""
     cfg, host, dev = layer
     budget = ("mass", 0.75)
     st, idx, cnt = _gpu_predict(cfg, dev, budget)
     heads = _sample_heads(cfg)
-    _check_heads(cfg, host, st, idx, cnt, budget, heads)
-    _check_attention_rows(cfg, host, dev, idx, cnt, heads)
+    qd, kd, vd = dev
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    o = torch.empty_like(qd)
+    lse = torch.empty((cfg.B, cfg.H, cfg.L), dtype=torch.float32, device="cuda")
+    ws_bytes = M.mod_attn_workspace_bytes(shape)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    M.mod_block_sparse_attn_fwd(shape, qd, kd, vd, idx, cnt, 0.0, o, lse, ws, ws_bytes)
+    torch.cuda.synchronize()
+    out = {h: (bf16_to_f64(o[0, h]), lse[0, h].cpu().numpy().astype(np.float64)) for h in heads}
+    yield cfg, host, st, idx, cnt, budget, heads, out
     st.close()
+
+
+def test_720p_mass_budget(mass_run):
+    """Selection parity on every query block of two heads per head type."""
+    cfg, host, st, idx, cnt, budget, heads, _ = mass_run
+    _check_heads(cfg, host, st, idx, cnt, budget, heads)
+
+
+@pytest.mark.parametrize("slot", range(6))
+def test_720p_mass_attention_whole_head(mass_run, slot):
+    """Attention parity on every query block of one sampled head (the
+    persistent work-groups steal across the XCD lists only at this size)."""
+    cfg, host, st, idx, cnt, budget, heads, out = mass_run
+    h = heads[slot]
+    rows = gpu_lists(idx[:, h:h + 1], cnt[:, h:h + 1])[0][0]
+    qf, kf, vf = (W.bf16_bits_to_f64(x[0, h]) for x in host)
+    Oo, Lo = O.attention(qf, kf, vf, rows, cfg.block, 1.0 / math.sqrt(cfg.d))
+    og, lg = out[h]
+    worst = 0.0
+    for i in range(cfg.n):
+        sl = slice(i * cfg.block, min(cfg.L, (i + 1) * cfg.block))
+        mx, mean = attention_errors(og[sl], Oo[sl])
+        assert mx <= MAX_ABS and mean <= MEAN_ABS, (h, i, mx, mean)
+        worst = max(worst, mx)
+    mx, mean = attention_errors(og, Oo)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS
+    assert np.abs(lg - Lo).max() <= LSE_ABS
+    print(f"head {h}: {cfg.n} query blocks, max-abs {mx:.2e}, mean-abs {mean:.2e}")
 
 
 @pytest.mark.parametrize("density", [0.5, 0.1, 0.05])

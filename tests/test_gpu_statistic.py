@@ -2,11 +2,19 @@
 its block-level reconstruction (Eq. 5) through the C ABI.
 
 The count of probabilities reaching eta is an integer decided in floating
-point; the GPU decides in fp32 (s >= (lse + log eta) / scale) and the oracle in
-fp64 against the GPU's own lse, so per block the counts may differ only by
-entries whose log-probability lies within TOL of log(eta).  The fit, the
-extrapolation and the selection are then checked against the oracle fed
-with the GPU's statistic (decoupled from those boundary entries)."""
+point: the GPU decides in fp32 (s >= (lse + log eta) / scale, with its own
+fp32 lse) and the oracle in fp64 with its own fp64 lse.  Per block the
+counts may differ only by entries whose fp64 log-probability lies within
+TOL + (the head's measured lse error) of log(eta).
+
+Two schedules:
+* GPU-fed: the oracle's fit, extrapolation and selection run on the GPU's
+  stored statistic, which isolates those steps (fit within 1e-9);
+* own chain: the oracle runs the whole chain on its own numbers (its own
+  lse, counts, reconstruction and fit); the GPU's lists must then match
+  under the gap rule widened by how far the undecided entries can move the
+  scores (a bound propagated through the linear fit and the extrapolation).
+"""
 import math
 
 import numpy as np
@@ -14,7 +22,7 @@ import pytest
 
 import oracle as O
 import workloads as W
-from parity import bf16_tensor, compare_lists, gpu_lists
+from parity import GAP, LSE_ABS, bf16_tensor, compare_lists, gpu_lists
 
 import paper_2601_11641_amd as M
 
@@ -68,16 +76,34 @@ def _attention(cfg, dev, idx, cnt):
     return lse
 
 
+def _oracle_counts(qf, kf, rows, cfg, lse_gpu, query_rows=None):
+    """The oracle's own statistic of one head (its own fp64 lse) and, per
+    block, the entries it cannot decide against the GPU: those within TOL +
+    max |lse_gpu - lse_oracle| of log(eta).  Returns (I, amb, lse error)."""
+    scale = 1.0 / math.sqrt(cfg.d)
+    _, _, lse_o = O.attention_statistic(qf, kf, rows, cfg.block, scale, ETA, rows=query_rows,
+                                        return_lse=True)
+    sel = ~np.isnan(lse_o)
+    err = float(np.abs(lse_gpu[sel] - lse_o[sel]).max())
+    assert err <= LSE_ABS, err
+    I, amb = O.attention_statistic(qf, kf, rows, cfg.block, scale, ETA, tol=TOL + err,
+                                   rows=query_rows)
+    return I, amb, err
+
+
 def _check_counts(cfg, host, lse, rows, stat_before, stat_after):
-    """Listed blocks: counts within the boundary entries; others unchanged."""
+    """Listed blocks: counts within the undecided entries of the oracle's own
+    statistic; others unchanged.  Returns the per-block radius of the
+    stored statistic's uncertainty from this update (undecided entries /
+    block size; NaN for unlisted blocks) [B, H, n, n]."""
     n = cfg.n
     sizes = O.block_sizes(cfg.L, cfg.block)
     lg = lse.cpu().numpy().astype(np.float64)
+    rad = np.full((cfg.B, cfg.H, n, n), np.nan)
     for b in range(cfg.B):
         for h in range(cfg.H):
             qf, kf = W.bf16_bits_to_f64(host[0][b, h]), W.bf16_bits_to_f64(host[1][b, h])
-            I, amb = O.attention_statistic(qf, kf, rows[b][h], cfg.block, 1.0 / math.sqrt(cfg.d), ETA,
-                                           lse=lg[b, h], tol=TOL)
+            I, amb, _ = _oracle_counts(qf, kf, rows[b][h], cfg, lg[b, h])
             listed = ~np.isnan(I)
             got = stat_after[b, h]
             cnt_diff = np.abs(got - np.nan_to_num(I)) * np.outer(sizes, sizes)
@@ -85,10 +111,36 @@ def _check_counts(cfg, host, lse, rows, stat_before, stat_after):
                 (b, h, float(cnt_diff[listed].max()), int(amb[listed].max()))
             if stat_before is not None:
                 assert (got[~listed] == stat_before[b, h][~listed]).all()
+            rad[b, h][listed] = amb[listed] / np.outer(sizes, sizes)[listed]
+    return rad
+
+
+class _ScoreBound:
+    """How far the scores of a prediction can move when the statistic of
+    every block b moves by at most radius(b): the fit is linear (minimum-norm
+    least squares, X = N+ M^T vec(I)) and so are the scores
+    sigma(i, j) = n (c[j - i] + d[j]) and the extrapolation, so
+    |d sigma(i, j)| <= sum_b |d sigma(i, j) / d I(b)| radius(b)."""
+
+    def __init__(self, n, regions):
+        self.n = n
+        Msys = O.design_matrix(n, regions)
+        self.Bm = O.solve_min_norm(O.normal_matrix(n, regions), Msys.T, n, len(regions))
+
+    def sigma(self, radius):
+        n, r = self.n, radius.ravel()
+        out = np.empty((n, n))
+        for j in range(n):
+            cidx = j - np.arange(n) + n - 1
+            out[:, j] = np.abs(n * (self.Bm[cidx] + self.Bm[2 * n - 1 + j][None, :])) @ r
+        return out
+
+    def coeffs(self, radius):
+        return np.abs(self.Bm) @ radius.ravel()
 
 
 @pytest.mark.parametrize("name", sorted(CONFIGS))
-def test_statistic_schedule(name):
+def test_statistic_schedule_gpu_fed(name):
     """Dense warm-up updates at steps 1 and 2, predictions at 3..5, a sparse
     re-anchor update at step 4 (Eq. 5: only the listed blocks change), and
     the masks of every predicted step against the oracle fed with the
@@ -199,9 +251,89 @@ def test_statistic_720p_dense_sampled_rows():
         sub = W.generate_heads(cfg, heads=[h])
         qf, kf = W.bf16_bits_to_f64(sub[0][0, 0]), W.bf16_bits_to_f64(sub[1][0, 0])
         rows = sorted(set(rng.choice(n - 1, size=3, replace=False).tolist()) | {n - 1})
-        I, amb = O.attention_statistic(qf, kf, [list(range(n))] * n, cfg.block, 1.0 / math.sqrt(cfg.d),
-                                       ETA, lse=lg[0, h], tol=TOL, rows=rows)
+        I, amb, err = _oracle_counts(qf, kf, [list(range(n))] * n, cfg, lg[0, h], query_rows=rows)
         for i in rows:
             diff = np.abs(got[0, h, i] - I[i]) * sizes[i] * sizes
             assert (diff <= amb[i] + 1e-6).all(), (h, i, float(diff.max()))
+        print(f"720p head {h}: lse error {err:.2e}, undecided entries {int(amb[rows].sum())} "
+              f"of {int(sizes[rows].sum()) * cfg.L}")
+    st.close()
+
+
+@pytest.mark.parametrize("name", sorted(CONFIGS))
+def test_statistic_schedule_own_chain(name):
+    """The oracle runs the whole statistic-1 chain on its own numbers: dense
+    updates at steps 1, 2 (its own fp64 lse and counts), predictions at 3..5,
+    a sparse re-anchor update at step 4 on its own lists (which the GPU
+    update is given too).  Counts agree up to the undecided entries; the
+    fitted coefficients and the lists agree up to what those entries can
+    move (propagated through the reconstruction of Eq. 5, the fit and the
+    extrapolation of Section 5.2); every differing row is excused only if it
+    satisfies the selection invariants at that tolerance."""
+    cfg = CONFIGS[name]
+    host, dev = _device(cfg)
+    qd, kd, _ = dev
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    params = dict(warmup_m=2, delta_t=2, tau_e=0.0)
+    st = M.Stats(shape, M.make_params(statistic="attention", eta=ETA, **params))
+    n, B, H = st.n, cfg.B, cfg.H
+    qf, kf = W.bf16_bits_to_f64(host[0]), W.bf16_bits_to_f64(host[1])
+    P = O.Predictor(B, H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens, statistic="attention", eta=ETA,
+                    **params)
+    sb = _ScoreBound(n, P.regions)
+    radius = np.zeros((B, H, n, n))           # uncertainty of the stored map per block
+    anchors = []                              # (step, radius of the map fitted at that step)
+    full = [[[list(range(n))] * n for _ in range(H)] for _ in range(B)]
+    fidx, fcnt = _lists_tensors(cfg, full)
+
+    def update(t, rows, idx, cnt, before):
+        lse = _attention(cfg, dev, idx, cnt)
+        M.mod_update_stats(st.handle, qd, kd, lse, idx, cnt, t)
+        torch.cuda.synchronize()
+        after = M.mod_stats_get_block_mass(st.handle, B, H, n)
+        rad = _check_counts(cfg, host, lse, rows, before, after)
+        listed = ~np.isnan(rad)
+        radius[listed] = rad[listed]          # Eq. 5: listed blocks replaced, others kept
+        P.update(qf, kf, rows, t)             # the oracle's own chain
+        anchors.append((t, radius.copy()))
+        X, t2 = M.mod_stats_get_anchor(st.handle, 0, B, H, st.p)
+        assert t2 == t
+        for b in range(B):
+            for h in range(H):
+                tol = sb.coeffs(radius[b, h]) + 1e-9 * max(1.0, np.abs(P.anchors[-1][1][b, h]).max())
+                assert (np.abs(X[b, h] - P.anchors[-1][1][b, h]) <= tol).all(), (t, b, h)
+        return after
+
+    before = None
+    for t in (1, 2):
+        before = update(t, full, fidx, fcnt, before)
+    idx = torch.empty((B, H, n, n), dtype=torch.int32, device="cuda")
+    cnt = torch.empty((B, H, n), dtype=torch.int32, device="cuda")
+    k = O.topk_count(0.4, n)
+    total = excused = 0
+    widest = 0.0
+    for t in (3, 4, 5):
+        M.mod_predict_block_mask(st.handle, None, None, t, M.make_budget("topk", density=0.4), idx, cnt)
+        torch.cuda.synchronize()
+        sel = P.predict(None, None, t, O.Budget("topk", density=0.4))
+        rows = gpu_lists(idx, cnt)
+        po = P.prediction(t)
+        (t1, r1), (t2, r2) = anchors[-2], anchors[-1]
+        w = (t - t2) / (t2 - t1)
+        for b in range(B):
+            for h in range(H):
+                dsig = abs(1 + w) * sb.sigma(r2[b, h]) + abs(w) * sb.sigma(r1[b, h])
+                gap = GAP + 2.0 * dsig.max(axis=1)
+                widest = max(widest, float(gap.max()))
+                sig = O.scores(*po[b][h], n)
+                forced = O.forced_mask(n, P.regions, bool(P.gates[b, h]))
+                nr, _, nx, bad = compare_lists(rows[b][h], sel[b][h], sig, forced, "topk", k, gap=gap)
+                assert not bad, (t, b, h, bad[:10])
+                total, excused = total + nr, excused + nx
+        if t == 4:                            # re-anchor on the oracle's own lists
+            olists = [[[r.kept.tolist() for r in sel[b][h]] for h in range(H)] for b in range(B)]
+            oidx, ocnt = _lists_tensors(cfg, olists)
+            before = update(t, olists, oidx, ocnt, before)
+    print(f"{name}: {excused} of {total} rows excused, widest gap {widest:.2e}")
+    assert excused <= max(2, 0.05 * total), (excused, total)
     st.close()
