@@ -57,14 +57,26 @@ WORKLOADS = {
     # 256 text tokens after the video (token-type-aware masking): 931 blocks
     "hunyuan-720p-text256": ("hunyuan+text256", "mass", 0.75),
     "small": ("small", "topk", 0.25),
+    "small-d50": ("small", "topk", 0.50),
+    "small-d100": ("small", "topk", 1.0),
+    # one GPU's share when a layer is sharded by head over 8 GPUs
+    "hunyuan-720p-h3": ("hunyuan@h3", "mass", 0.75),
+    "wan-720p-h5": ("wan@h5", "mass", 0.75),
 }
 
 
 def layer_config(W, name):
-    """A layer of the workload set; "<layer>+text<T>" appends T text tokens."""
+    """A layer of the workload set; "<layer>+text<T>" appends T text tokens,
+    "<layer>@h<H>" keeps its first H heads (one GPU's share of a layer
+    sharded by head)."""
+    name, _, heads = name.partition("@h")
     base, _, text = name.partition("+text")
     cfg = W.CONFIGS[base]
-    return W.with_text(cfg, int(text)) if text else cfg
+    if text:
+        cfg = W.with_text(cfg, int(text))
+    if heads:
+        cfg = W.with_heads(cfg, int(heads))
+    return cfg
 WARMUP_M = 5          # dense warm-up steps before the timed sparse steps
 
 
@@ -88,6 +100,12 @@ def parse():
                     help="50-step denoising schedule on the Hunyuan 720p shape (5 dense warm-up "
                          "steps, 45 predicted sparse steps) for re-anchor intervals 10 and 1; one "
                          "JSON line per interval")
+    ap.add_argument("--share", action="store_true",
+                    help="one GPU's share of a layer sharded by head over 8 GPUs (Hunyuan 3 of 24 "
+                         "heads, Wan 5 of 40) against the whole layer on the same GPU, mass 0.75: "
+                         "attention time, rate, per-head imbalance and the share's time over the "
+                         "kept-work-proportional part of the whole layer's time; one JSON line "
+                         "per layer")
     ap.add_argument("--trace-summary", nargs=2, metavar=("STATS_CSV", "BENCH_LOG"),
                     help="format a rocprofv3 --kernel-trace --stats CSV of a bench run (and the JSON "
                          "line that run printed) into profiles/hunyuan720p_step_kernel_stats.md and exit")
@@ -373,8 +391,10 @@ def run_sweep(args):
             step[0] += 1               # delta_t = 1: every call re-anchors at a new step
             M.mod_predict_block_mask(st.handle, qd, kd, step[0], budget, kv_idx, kv_cnt, stream)
         pred_ms = _median_ms(predict, 5, stream)
+        ws_bytes = M.mod_attn_workspace_bytes(shape)
+        ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
         attn = lambda: M.mod_block_sparse_attn_fwd(shape, qd, kd, vd, kv_idx, kv_cnt, 0.0, out,  # noqa: E731
-                                                   None, None, 0, stream)
+                                                   None, ws, ws_bytes, stream)
         for _ in range(args.warmup):
             attn()
         attn_ms = _median_ms(attn, max(args.steps, 5), stream)
@@ -398,6 +418,74 @@ def run_sweep(args):
     print(json.dumps({"fit": "attn_ms = a + b * kept_tflop", "a_ms": round(float(a), 3),
                       "b_ms_per_tflop": round(float(b), 4), "r2": round(r2, 5),
                       "marginal_tflops": round(1e3 / float(b), 1)}), flush=True)
+
+
+def _layer_attention(M, W, cfg, mode, val, args, dev):
+    """Predicted lists (re-anchor step) and the attention's median time on
+    one layer; returns (attn_ms, kept flop per head)."""
+    import numpy as np
+    import torch
+    host = W.generate(cfg)
+    qd, kd, vd = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev) for x in host)
+    del host
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    stream = torch.cuda.current_stream()
+    st = M.Stats(shape, M.make_params(warmup_m=WARMUP_M, delta_t=1))
+    n = st.n
+    kv_idx = torch.empty((cfg.B, cfg.H, n, n), dtype=torch.int32, device=dev)
+    kv_cnt = torch.empty((cfg.B, cfg.H, n), dtype=torch.int32, device=dev)
+    M.mod_collect_stats(st.handle, qd, kd, WARMUP_M - 1)
+    M.mod_collect_stats(st.handle, qd, kd, WARMUP_M)
+    budget = M.make_budget(mode, density=val) if mode == "topk" else M.make_budget(mode, mass=val)
+    M.mod_predict_block_mask(st.handle, qd, kd, WARMUP_M + 1, budget, kv_idx, kv_cnt, stream)
+    out = torch.empty_like(qd)
+    ws_bytes = M.mod_attn_workspace_bytes(shape)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    attn = lambda: M.mod_block_sparse_attn_fwd(shape, qd, kd, vd, kv_idx, kv_cnt, 0.0, out,  # noqa: E731
+                                               None, ws, ws_bytes, stream)
+    for _ in range(args.warmup):
+        attn()
+    attn_ms = _median_ms(attn, max(args.steps, 5), stream)
+    per_head = np.array([kept_flops(kv_idx[:, h:h + 1], kv_cnt[:, h:h + 1], cfg.L, cfg.block, cfg.d)
+                         for h in range(cfg.H)])
+    st.close()
+    return attn_ms, per_head
+
+
+def run_share(args):
+    """One GPU's share of a layer sharded by head over 8 GPUs, against the
+    whole layer on the same GPU (mass 0.75).  makespan_vs_ideal is the
+    share's attention time over the whole layer's time scaled by the
+    share's fraction of the kept work: 1.0 means the share runs at the whole
+    layer's rate, above 1 means the fewer, unevenly dense heads leave part
+    of the chip idle."""
+    import numpy as np
+    import torch
+
+    import paper_2601_11641_amd as M
+    import workloads as W
+
+    dev = torch.device("cuda:0")
+    for base, H in (("hunyuan", 3), ("wan", 5)):
+        full = W.CONFIGS[base]
+        t_full, w_full = _layer_attention(M, W, full, "mass", 0.75, args, dev)
+        share = W.with_heads(full, H)
+        t_share, w_share = _layer_attention(M, W, share, "mass", 0.75, args, dev)
+        assert np.allclose(w_share, w_full[:H])       # the share's heads are the layer's first H
+        ideal = t_full * w_share.sum() / w_full.sum()
+        print(json.dumps({
+            "workload": f"{base}-720p share: heads 0..{H - 1} of {full.H} (B=1 L={full.L} d={full.d} "
+                        f"block={full.block}), mass 0.75",
+            "share_attn_ms": round(t_share, 3),
+            "share_kept_tflop": round(float(w_share.sum()) / 1e12, 3),
+            "share_attn_tflops": round(float(w_share.sum()) / (t_share * 1e-3) / 1e12, 1),
+            "share_frac": round(float(w_share.sum()) / (t_share * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "share_head_density": [round(float(x) / (4.0 * full.d * full.L * full.L), 4) for x in w_share],
+            "share_head_imbalance": round(float(w_share.max() / w_share.mean()), 3),
+            "layer_attn_ms": round(t_full, 3),
+            "layer_attn_tflops": round(float(w_full.sum()) / (t_full * 1e-3) / 1e12, 1),
+            "makespan_vs_ideal": round(t_share / ideal, 3),
+        }), flush=True)
 
 
 def run_schedule(args):
@@ -526,6 +614,9 @@ def main():
         return
     if args.schedule:
         run_schedule(args)
+        return
+    if args.share:
+        run_share(args)
         return
 
     import numpy as np

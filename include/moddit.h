@@ -196,12 +196,19 @@ mod_status mod_predict_block_mask(mod_stats* stats, const void* q, const void* k
                                   const mod_budget* budget, int32_t* kv_idx, int32_t* kv_cnt,
                                   void* stream);
 
-/* Device workspace the attention call needs, in bytes (about
- * 4 * (B * H * (n/2 + 11) + 288); 0 for an invalid shape).  It holds the call's work
- * plan: the (head, pair of query blocks) items ordered and spread over the
- * chip by their list lengths.  Owned by the caller, rewritten by every call;
+/* Device workspace of the attention call, in bytes (0 for an invalid
+ * shape): its work plan -- the (head, pair of query blocks) items ordered
+ * and spread over the chip by their list lengths, rewritten by every call --
+ * and room for the split-KV path (below): up to 1024 slots of partial
+ * results of 8 * block * (d + 1) bytes each, fewer for short sequences
+ * (none when n <= 64).  About 4 * (B*H*(n/2 + 16) + 300) bytes plus the
+ * slots (47 KB + 135 MB at the 720p Hunyuan layer).  Owned by the caller;
  * two calls in flight at once need two workspaces. */
 size_t mod_attn_workspace_bytes(const mod_shape* shape);
+
+/* The smallest workspace the attention call accepts: the work plan alone
+ * (the call then never splits a walk).  0 for an invalid shape. */
+size_t mod_attn_plan_bytes(const mod_shape* shape);
 
 /* Block-sparse attention forward (Eq. 1 with the block mask of the lists):
  * for every query token p of block i of head (b,h),
@@ -214,9 +221,18 @@ size_t mod_attn_workspace_bytes(const mod_shape* shape);
  * kv_cnt = 0 gives O = 0 and lse = -inf.  scale = 0 means 1/sqrt(d).
  * q, k, v, o: [B,H,L,d] bf16 device; lse: [B,H,L] fp32 device or NULL.
  * bf16 MFMA products, fp32 softmax and accumulation.  `frame_tokens` and
- * `text_tokens` of the shape are not used.  workspace: device memory of at
- * least mod_attn_workspace_bytes(shape) bytes (ws_bytes), 16-byte aligned,
- * else MOD_ERR_INVALID_ARG. */
+ * `text_tokens` of the shape are not used.  workspace: device memory of
+ * ws_bytes bytes, 16-byte aligned, at least mod_attn_plan_bytes(shape),
+ * else MOD_ERR_INVALID_ARG.
+ * Split-KV: when few pairs carry long walks (few heads, dense rows), a pair
+ * whose work exceeds half of a compute unit's share of the launch is split
+ * into chunks of its walk, processed as separate items that write O / l and
+ * LSE per row in fp32 into the workspace's slots; a merge kernel then
+ * combines them (LSE = log sum_c exp(lse_c), O = sum_c exp(lse_c - LSE) O_c)
+ * in chunk order, so the result is deterministic for given lists.  With
+ * fewer than two slots (a workspace of mod_attn_plan_bytes) nothing is
+ * split; whether a pair is split depends on the lists of all heads, so
+ * outputs may differ by rounding between a split and an unsplit run. */
 mod_status mod_block_sparse_attn_fwd(const mod_shape* shape, const void* q, const void* k,
                                      const void* v, const int32_t* kv_idx,
                                      const int32_t* kv_cnt, float scale, void* o, float* lse,
@@ -227,9 +243,10 @@ mod_status mod_block_sparse_attn_fwd(const mod_shape* shape, const void* q, cons
  * allocation): mod_block_sparse_attn_fwd with its work plan held in a
  * library-owned device array of MOD_ATTN_NOALLOC_MAX_BYTES per device
  * instead of a caller workspace.  Same arguments, layout, numerics and
- * errors as mod_block_sparse_attn_fwd (its output is bit-identical);
- * shapes whose workspace, mod_attn_workspace_bytes(shape), exceeds the
- * array are rejected with MOD_ERR_UNSUPPORTED.  The call allocates nothing:
+ * errors as mod_block_sparse_attn_fwd given a workspace of
+ * mod_attn_plan_bytes(shape) bytes (its output is bit-identical to that
+ * call's: no walk is split); shapes whose plan exceeds the array are
+ * rejected with MOD_ERR_UNSUPPORTED.  The call allocates nothing:
  * the array is a static device variable whose address is resolved on the
  * first call on each device (the current device, which must be the device
  * of the pointers and the stream) and kept until the process ends.  Every

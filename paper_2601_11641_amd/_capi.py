@@ -72,6 +72,7 @@ _SIGS = {
     "mod_predict_block_mask": (c_int, [c_void_p, c_void_p, c_void_p, c_int, POINTER(mod_budget),
                                        c_void_p, c_void_p, c_void_p]),
     "mod_attn_workspace_bytes": (c_size_t, [POINTER(mod_shape)]),
+    "mod_attn_plan_bytes": (c_size_t, [POINTER(mod_shape)]),
     "mod_block_sparse_attn_fwd": (c_int, [POINTER(mod_shape), c_void_p, c_void_p, c_void_p,
                                           c_void_p, c_void_p, c_float, c_void_p, c_void_p,
                                           c_void_p, c_size_t, c_void_p]),
@@ -196,6 +197,10 @@ def mod_predict_block_mask(stats, q, k, step: int, budget: mod_budget, kv_idx, k
 
 def mod_attn_workspace_bytes(shape: mod_shape) -> int:
     return int(_lib.mod_attn_workspace_bytes(_ref(shape)))
+
+
+def mod_attn_plan_bytes(shape: mod_shape) -> int:
+    return int(_lib.mod_attn_plan_bytes(_ref(shape)))
 
 
 def mod_block_sparse_attn_fwd(shape: mod_shape, q, k, v, kv_idx, kv_cnt, scale: float, o,

@@ -210,190 +210,255 @@ __device__ __forceinline__ void wait_vmcnt() {
 // ---------------------------------------------------------------------------
 // Work plan.  The per-pair work (about the two rows' list lengths) varies
 // along the sequence and across heads, so a fixed pair -> XCD map leaves
-// some XCDs idle at the end.  Three small kernels write a plan into the
-// workspace before every attention launch:
-//   split  per head, the cost 4 + cnt(2p) + cnt(2p+1) of every pair p and
-//          eight contiguous pair ranges of about equal cost (pair p goes to
-//          range floor(8 * midpoint(p) / total)), one per XCD: neighbouring
-//          rows share K/V blocks, so an XCD's L2 serves its range;
-//   order  heads by decreasing total cost (ties by index; natural order
-//          above kPlanMaxHeads heads);
-//   lists  per XCD, its ranges of all heads in that order, as a list of
-//          items bh * npairs + p, plus its length, start and a zeroed
-//          fetch counter; the list is then bucket-sorted by decreasing cost
-//          (lists longer than kPlanSortMax keep the head order).
+// some XCDs idle at the end.  One small kernel (one work-group per XCD, each
+// computing the shared quantities itself) writes a plan into the workspace
+// before every attention launch:
+//   costs  the cost 4 + cnt(2p) + cnt(2p+1) of every pair p of every head;
+//          per head, eight contiguous pair ranges of about equal cost (pair
+//          p goes to range floor(8 * midpoint(p) / head total)), one per XCD:
+//          neighbouring rows share K/V blocks, so an XCD's L2 serves its
+//          range, and all XCDs work through the same heads at once;
+//   split  a pair whose cost exceeds half of the average per-CU load
+//          W / (compute units) is split into C chunks of its walk (the walk
+//          of a pair has max(cnt(2p), cnt(2p+1)) steps: the blocks of both
+//          lists, then the one-list blocks of both rows side by side), each
+//          of about an eighth of that load and at least kMinChunkSteps
+//          steps; the chunks become separate items writing partial results
+//          (fp32 O / l and LSE per row) into workspace slots, merged after
+//          the launch in chunk order.  If the slots do not suffice, the
+//          chunk length doubles until they do (or nothing is split);
+//   lists  per XCD, the items of its ranges in head-major order (a chunk
+//          item is the slot number with bit 30 set), its length, start and
+//          a zeroed fetch counter; each list is then bucket-sorted by
+//          decreasing cost (lists longer than kPlanSortMax keep the head
+//          order), so long items start early instead of ending the launch
+//          late.
+// Every work-group computes the same split decision and slot numbering from
+// the same counts, so the plan is deterministic; only the order of equal-
+// cost items within a bucket varies, which affects timing, not results.
 // The attention work-groups are persistent (one per CU): a work-group
 // fetches the next item of its XCD's list with an atomic counter and, once
 // that list is drained, of the other XCDs' lists, until all are drained.
 // Each counter has a 128-byte line of its own, so the XCDs' atomics do not
 // queue on one line.
 // ---------------------------------------------------------------------------
-constexpr int kPlanThreads = 256;
-constexpr int kPlanMaxHeads = 4096;
+constexpr int kPlanThreads = 1024;
 constexpr int kCtrStride = 32;        // ints between fetch counters (one 128-byte line each)
-constexpr int kPlanHdr = 8 * kCtrStride + 32;   // ints: ctr[8] (strided), len[8], start[8], pad
+constexpr int kPlanHdr = 8 * kCtrStride + 32;   // ints: ctr[8] (strided), len[8], start[8], misc[8]
 constexpr int kPlanSortMax = 8192;    // longer XCD lists keep the head order
 constexpr int kPlanBuckets = 512;
+constexpr int kChunkBit = 1 << 30;    // item flag: a chunk of a split pair (slot in the low bits)
+constexpr int kMinChunkSteps = 64;    // shortest chunk of a split walk
+constexpr int kMaxSplitSlots = 1024;  // partial-result slots a workspace holds at most
 
+// Work-plan layout in the workspace (ints, then the partial-result slots).
 struct Plan {
-    int* ctr;       // fetch counters, ctr[kCtrStride * x] for XCD x
-    int* len;       // [8] items per XCD list
-    int* start;     // [8] first item of each XCD list in `items`
-    int* tot;       // [BH] total cost per head
-    int* order;     // [BH] heads by decreasing cost
-    int* bounds;    // [BH][9] pair ranges per XCD
-    int* items;     // [BH * npairs]
-    __host__ __device__ Plan(void* ws, int BH) {
+    int* ctr;           // fetch counters, ctr[kCtrStride * x] for XCD x
+    int* len;           // [8] items per XCD list
+    int* start;         // [8] first item of each XCD list in `items`
+    int* misc;          // [0] split pairs, [1] chunk length in steps (0: none)
+    long long* headpre; // [8][BH + 1] per work-group: cost before each head's first pair
+    int* items;         // [BH * npairs + S]
+    int4* chunks;       // [S] chunk items: {pair, first step, end step, 0}
+    int4* splits;       // [S] split pairs: {pair, chunks, first slot, 0}
+    float* part;        // [S] slots of partial results
+    __host__ __device__ static size_t ints(int BH, int npairs, int S) {
+        size_t w = (size_t)kPlanHdr + 2 * 8 * ((size_t)BH + 1) + (size_t)BH * npairs + S;
+        w = (w + 3) / 4 * 4 + 8 * (size_t)S;
+        return (w + 63) / 64 * 64;
+    }
+    __host__ __device__ Plan(void* ws, int BH, int npairs, int S) {
         int* w = static_cast<int*>(ws);
         ctr = w;
         len = w + 8 * kCtrStride;
         start = len + 8;
-        tot = w + kPlanHdr;
-        order = tot + BH;
-        bounds = order + BH;
-        items = bounds + 9 * BH;
+        misc = start + 8;
+        headpre = reinterpret_cast<long long*>(w + kPlanHdr);
+        items = w + kPlanHdr + 2 * 8 * ((size_t)BH + 1);
+        size_t o = (size_t)kPlanHdr + 2 * 8 * ((size_t)BH + 1) + (size_t)BH * npairs + S;
+        o = (o + 3) / 4 * 4;
+        chunks = reinterpret_cast<int4*>(w + o);
+        splits = chunks + S;
+        part = reinterpret_cast<float*>(w + ints(BH, npairs, S));
     }
 };
+
+// Floats per partial-result slot: O / l for the BS x D rows of both query
+// blocks of a pair, then their LSE.
+__host__ __device__ constexpr size_t slot_floats(int D, int BS) { return 2 * (size_t)BS * D + 2 * (size_t)BS; }
 
 __device__ __forceinline__ int clamp_count(const int32_t* kv_cnt, size_t row, int n) {
     return min(max(kv_cnt[row], 0), n);
 }
 
-__global__ __launch_bounds__(kPlanThreads) void plan_split_kernel(const int32_t* __restrict__ kv_cnt,
-                                                                  void* ws, int BH, int n) {
-    __shared__ int scan[kPlanThreads];
-    __shared__ int below[kXcds];
-    const Plan pl(ws, BH);
-    const int bh = blockIdx.x, t = threadIdx.x;
-    const int npairs = (n + 1) / 2;
-    const int per = (npairs + kPlanThreads - 1) / kPlanThreads;   // pairs per thread, contiguous
-    auto cost = [&](int p) {
-        const size_t r0 = (size_t)bh * n + 2 * p;
-        return 4 + clamp_count(kv_cnt, r0, n) + (2 * p + 1 < n ? clamp_count(kv_cnt, r0 + 1, n) : 0);
-    };
-    int mine = 0;
-    for (int e = 0; e < per; ++e) {
-        const int p = t * per + e;
-        if (p < npairs) mine += cost(p);
-    }
-    scan[t] = mine;
-    if (t < kXcds) below[t] = 0;
-    __syncthreads();
-    for (int off = 1; off < kPlanThreads; off <<= 1) {   // inclusive scan
-        const int y = t >= off ? scan[t - off] : 0;
-        __syncthreads();
-        scan[t] += y;
-        __syncthreads();
-    }
-    const int total = scan[kPlanThreads - 1];
-    int run = scan[t] - mine;                               // cost before this thread's pairs
-    int cnt[kXcds] = {};
-    for (int e = 0; e < per; ++e) {
-        const int p = t * per + e;
-        if (p >= npairs) break;
-        const int c = cost(p);
-        // range of the pair's midpoint: floor(8 * (run + c/2) / total)
-        const int x = (int)min<long long>(kXcds - 1, ((long long)(2 * run + c) * kXcds) / (2LL * total));
-        for (int xx = x + 1; xx < kXcds; ++xx) ++cnt[xx];  // pairs below range xx
-        run += c;
-    }
-    for (int xx = 1; xx < kXcds; ++xx)
-        if (cnt[xx]) atomicAdd(&below[xx], cnt[xx]);
-    __syncthreads();
-    if (t == 0) {
-        int* b = pl.bounds + 9 * bh;
-        for (int xx = 0; xx < kXcds; ++xx) b[xx] = below[xx];
-        b[kXcds] = npairs;
-        pl.tot[bh] = total;
-    }
-}
-
-__global__ __launch_bounds__(kPlanThreads) void plan_order_kernel(void* ws, int BH) {
-    const Plan pl(ws, BH);
-    const int h = blockIdx.x * kPlanThreads + threadIdx.x;
-    if (h >= BH) return;
-    int rank = h;
-    if (BH <= kPlanMaxHeads) {
-        const int th = pl.tot[h];
-        rank = 0;
-        for (int o2 = 0; o2 < BH; ++o2) {
-            const int to = pl.tot[o2];
-            rank += (to > th || (to == th && o2 < h)) ? 1 : 0;
-        }
-    }
-    pl.order[rank] = h;
-}
-
-// one work-group per XCD list
-__global__ __launch_bounds__(kPlanThreads) void plan_lists_kernel(const int32_t* __restrict__ kv_cnt,
-                                                                  void* ws, int BH, int n) {
-    __shared__ int xtot[kXcds];
-    __shared__ int scan[kPlanThreads];
-    const Plan pl(ws, BH);
-    const int x = blockIdx.x, t = threadIdx.x;
-    const int npairs = (n + 1) / 2;
-    if (t < kXcds) xtot[t] = 0;
-    __syncthreads();
-    int part[kXcds] = {};
-    for (int h = t; h < BH; h += kPlanThreads) {
-        const int* b = pl.bounds + 9 * h;
-        for (int xx = 0; xx < kXcds; ++xx) part[xx] += b[xx + 1] - b[xx];
-    }
-    for (int xx = 0; xx < kXcds; ++xx)
-        if (part[xx]) atomicAdd(&xtot[xx], part[xx]);
-    __syncthreads();
-    int first = 0;
-    for (int xx = 0; xx < x; ++xx) first += xtot[xx];
-    // this XCD's range lengths in head order, blocked per thread, scanned
-    const int per = (BH + kPlanThreads - 1) / kPlanThreads;
-    int mine = 0;
-    for (int e = 0; e < per; ++e) {
-        const int s2 = t * per + e;
-        if (s2 < BH) {
-            const int* b = pl.bounds + 9 * pl.order[s2];
-            mine += b[x + 1] - b[x];
-        }
-    }
-    scan[t] = mine;
+// Work-group sums and exclusive scans over kPlanThreads threads.
+template <class T>
+__device__ T plan_scan(T v, T* buf, T& total) {
+    const int t = threadIdx.x;
+    buf[t] = v;
     __syncthreads();
     for (int off = 1; off < kPlanThreads; off <<= 1) {
-        const int y = t >= off ? scan[t - off] : 0;
+        const T y = t >= off ? buf[t - off] : T(0);
         __syncthreads();
-        scan[t] += y;
+        buf[t] += y;
         __syncthreads();
     }
-    int pos = first + scan[t] - mine;
-    for (int e = 0; e < per; ++e) {
-        const int s2 = t * per + e;
-        if (s2 >= BH) break;
-        const int h = pl.order[s2];
-        const int* b = pl.bounds + 9 * h;
-        for (int p = b[x]; p < b[x + 1]; ++p) pl.items[pos++] = h * npairs + p;
+    total = buf[kPlanThreads - 1];
+    const T ex = buf[t] - v;
+    __syncthreads();
+    return ex;
+}
+
+__global__ __launch_bounds__(kPlanThreads) void plan_kernel(const int32_t* __restrict__ kv_cnt, void* ws,
+                                                            int BH, int n, int ncu, int S) {
+    __shared__ long long scan64[kPlanThreads];
+    __shared__ int xcnt[kXcds];
+    const int x = blockIdx.x, t = threadIdx.x;
+    const int npairs = (n + 1) / 2;
+    const long long P = (long long)BH * npairs;
+    const Plan pl(ws, BH, npairs, S);
+    long long* hp = pl.headpre + (size_t)x * (BH + 1);
+    const long long per = (P + kPlanThreads - 1) / kPlanThreads;
+    const long long q0 = min(P, (long long)t * per), q1 = min(P, q0 + per);
+    struct Pair { int c0, c1; };
+    auto counts = [&](long long q) {
+        const int bh = (int)(q / npairs), p = (int)(q % npairs);
+        const size_t r0 = (size_t)bh * n + 2 * p;
+        return Pair{clamp_count(kv_cnt, r0, n), 2 * p + 1 < n ? clamp_count(kv_cnt, r0 + 1, n) : 0};
+    };
+    // cost before every pair (global order) and before every head
+    long long mine = 0;
+    for (long long q = q0; q < q1; ++q) {
+        const Pair c = counts(q);
+        mine += 4 + c.c0 + c.c1;
+    }
+    long long W = 0;
+    const long long pre = plan_scan<long long>(mine, scan64, W);
+    {
+        long long run = pre;
+        for (long long q = q0; q < q1; ++q) {
+            const Pair c = counts(q);
+            if (q % npairs == 0) hp[q / npairs] = run;
+            run += 4 + c.c0 + c.c1;
+        }
+        if (t == 0) hp[BH] = W;
+    }
+    __syncthreads();   // the head prefixes (this work-group's own copy) are visible
+    // split policy: chunks of cs steps for pairs costing more than half the
+    // per-CU load, cs doubled until the chunks fit the slots
+    const double A = (double)W / (double)max(ncu, 1);
+    long long cs = 0;
+    auto nchunks = [&](const Pair& c, long long csteps) -> long long {
+        const long long cost = 4 + c.c0 + c.c1;
+        const long long steps = max(c.c0, c.c1);
+        if (csteps <= 0 || (double)cost <= 0.5 * A || steps <= csteps) return 1;
+        return (steps + csteps - 1) / csteps;
+    };
+    if (S >= 2) {
+        cs = max((long long)kMinChunkSteps, (long long)(A / 8.0));
+        for (;;) {
+            long long need = 0;
+            for (long long q = q0; q < q1; ++q) {
+                const long long C = nchunks(counts(q), cs);
+                if (C > 1) need += C;
+            }
+            long long tot_need = 0;
+            (void)plan_scan<long long>(need, scan64, tot_need);
+            if (tot_need <= S) break;
+            cs *= 2;
+            if (cs > n) { cs = 0; break; }
+        }
+    }
+    // XCD of every pair: its head's cost range, by the pair's midpoint
+    auto xcd_of = [&](long long q, long long before, const Pair& c) {
+        const int h = (int)(q / npairs);
+        const long long tot = hp[h + 1] - hp[h];
+        const long long mid2 = 2 * (before - hp[h]) + 4 + c.c0 + c.c1;
+        return (int)min<long long>(kXcds - 1, (mid2 * kXcds) / (2 * tot));
+    };
+    long long cntx[kXcds] = {};
+    long long slots_mine = 0, splits_mine = 0;
+    {
+        long long run = pre;
+        for (long long q = q0; q < q1; ++q) {
+            const Pair c = counts(q);
+            const int xq = xcd_of(q, run, c);
+            const long long C = nchunks(c, cs);
+            cntx[xq] += C;
+            if (C > 1) {
+                slots_mine += C;
+                splits_mine += 1;
+            }
+            run += 4 + c.c0 + c.c1;
+        }
+    }
+    if (t < kXcds) xcnt[t] = 0;
+    __syncthreads();
+    for (int xx = 0; xx < kXcds; ++xx)
+        if (cntx[xx]) atomicAdd(&xcnt[xx], (int)cntx[xx]);
+    __syncthreads();
+    int first = 0;
+    for (int xx = 0; xx < x; ++xx) first += xcnt[xx];
+    const int lenx = xcnt[x];
+    long long dummy = 0;
+    const long long posx = plan_scan<long long>(cntx[x], scan64, dummy);
+    const long long slot0 = plan_scan<long long>(slots_mine, scan64, dummy);
+    long long nsplit = 0;
+    const long long split0 = plan_scan<long long>(splits_mine, scan64, nsplit);
+    // this XCD's items, head-major; the chunks of a split pair described
+    {
+        long long run = pre, pos = first + posx, slot = slot0, sidx = split0;
+        for (long long q = q0; q < q1; ++q) {
+            const Pair c = counts(q);
+            const int xq = xcd_of(q, run, c);
+            const long long C = nchunks(c, cs);
+            if (C == 1) {
+                if (xq == x) pl.items[pos++] = (int)q;
+            } else {
+                const long long steps = max(c.c0, c.c1);
+                if (xq == x) {
+                    pl.splits[sidx] = make_int4((int)q, (int)C, (int)slot, 0);
+                    for (long long cc = 0; cc < C; ++cc) {
+                        pl.chunks[slot + cc] = make_int4((int)q, (int)(cc * steps / C), (int)((cc + 1) * steps / C), 0);
+                        pl.items[pos++] = kChunkBit | (int)(slot + cc);
+                    }
+                }
+                slot += C;
+                sidx += 1;
+            }
+            run += 4 + c.c0 + c.c1;
+        }
     }
     if (t == 0) {
-        pl.len[x] = xtot[x];
+        pl.len[x] = lenx;
         pl.start[x] = first;
         pl.ctr[kCtrStride * x] = 0;
+        if (x == 0) {
+            pl.misc[0] = (int)nsplit;
+            pl.misc[1] = (int)cs;
+        }
     }
     // Longest items first: a bucket sort of the list by decreasing cost
     // (order within a bucket unspecified; the order only affects timing).
-    // The few items far above the rest (rows that keep every block) then
-    // start early instead of being left for the end of the launch.
-    const int len = xtot[x];
-    if (len > kPlanSortMax) return;
+    if (lenx > kPlanSortMax) return;
     __shared__ int vals[kPlanSortMax];
     __shared__ int cursor[kPlanBuckets];
     int shift = 0;
     while (((4 + 2 * n) >> shift) >= kPlanBuckets) ++shift;
     auto bucket = [&](int item) {
-        const int h = item / npairs, p = item % npairs;
-        const size_t r0 = (size_t)h * n + 2 * p;
-        const int c = 4 + clamp_count(kv_cnt, r0, n) + (2 * p + 1 < n ? clamp_count(kv_cnt, r0 + 1, n) : 0);
-        return (kPlanBuckets - 1) - (c >> shift);          // descending cost
+        int c;
+        if (item & kChunkBit) {
+            const int4 ch = pl.chunks[item & (kChunkBit - 1)];
+            c = 4 + 2 * (ch.z - ch.y);
+        } else {
+            const Pair pc = counts(item);
+            c = 4 + pc.c0 + pc.c1;
+        }
+        return (kPlanBuckets - 1) - min(kPlanBuckets - 1, c >> shift);   // descending cost
     };
     for (int bb = t; bb < kPlanBuckets; bb += kPlanThreads) cursor[bb] = 0;
-    __syncthreads();   // also: every item of the list has been written
-    for (int a = t; a < len; a += kPlanThreads) {
+    __syncthreads();   // also: every item (and chunk) of the list has been written
+    for (int a = t; a < lenx; a += kPlanThreads) {
         const int it = pl.items[first + a];
         vals[a] = it;
         atomicAdd(&cursor[bucket(it)], 1);
@@ -408,9 +473,70 @@ __global__ __launch_bounds__(kPlanThreads) void plan_lists_kernel(const int32_t*
         }
     }
     __syncthreads();
-    for (int a = t; a < len; a += kPlanThreads) {
+    for (int a = t; a < lenx; a += kPlanThreads) {
         const int it = vals[a];
         pl.items[first + atomicAdd(&cursor[bucket(it)], 1)] = it;
+    }
+}
+
+// Merge of split pairs: for every row of both query blocks of a split pair,
+// LSE = log sum_c exp(lse_c) and O = sum_c exp(lse_c - LSE) O_c over its
+// chunks c = 0 .. C-1 in order (rows no chunk reached: O = 0, LSE = -inf).
+// Persistent: work-group b takes (split pair, query block) b, b + grid, ...
+template <int D, int BS>
+__global__ __launch_bounds__(256) void merge_kernel(void* ws, int BH, int n, int S, int L,
+                                                    uint16_t* __restrict__ o, float* __restrict__ lse) {
+    constexpr int TPR = 256 / BS;          // threads per row
+    constexpr int DPT = D / TPR;           // d values per thread
+    const int npairs = (n + 1) / 2;
+    const Plan pl(ws, BH, npairs, S);
+    const int nsplit = pl.misc[0];
+    const int t = threadIdx.x, r = t / TPR, d0 = (t % TPR) * DPT;
+    for (int m = blockIdx.x; m < 2 * nsplit; m += gridDim.x) {
+        const int4 sp = pl.splits[m / 2];
+        const int g = m % 2, q = sp.x, C = sp.y;
+        const int bh = q / npairs, i = 2 * (q % npairs) + g;
+        const int row = i * BS + r;
+        if (i >= n || row >= L || q < 0 || bh >= BH || sp.z < 0 || sp.z + C > S) continue;
+        float lmax = -INFINITY;
+        for (int c = 0; c < C; ++c) {
+            const float* sl = pl.part + (size_t)(sp.z + c) * slot_floats(D, BS);
+            lmax = fmaxf(lmax, sl[2 * BS * D + g * BS + r]);
+        }
+        float acc[DPT];
+#pragma unroll
+        for (int e = 0; e < DPT; ++e) acc[e] = 0.0f;
+        float wsum = 0.0f;
+        if (lmax > -INFINITY) {
+            for (int c = 0; c < C; ++c) {
+                const float* sl = pl.part + (size_t)(sp.z + c) * slot_floats(D, BS);
+                const float lc = sl[2 * BS * D + g * BS + r];
+                const float wgt = lc > -INFINITY ? expf(lc - lmax) : 0.0f;
+                wsum += wgt;
+                const float4* src = reinterpret_cast<const float4*>(sl + ((size_t)g * BS + r) * D + d0);
+#pragma unroll
+                for (int e = 0; e < DPT / 4; ++e) {
+                    const float4 v4 = src[e];
+                    acc[4 * e] += wgt * v4.x;
+                    acc[4 * e + 1] += wgt * v4.y;
+                    acc[4 * e + 2] += wgt * v4.z;
+                    acc[4 * e + 3] += wgt * v4.w;
+                }
+            }
+        }
+        const float inv = wsum > 0.0f ? 1.0f / wsum : 0.0f;
+        uint16_t* orow = o + ((size_t)bh * L + row) * D + d0;
+#pragma unroll
+        for (int e = 0; e < DPT / 4; ++e) {
+            uint2 pk;
+            pk.x = (uint32_t)__builtin_bit_cast(uint16_t, static_cast<__bf16>(acc[4 * e] * inv)) |
+                   ((uint32_t)__builtin_bit_cast(uint16_t, static_cast<__bf16>(acc[4 * e + 1] * inv)) << 16);
+            pk.y = (uint32_t)__builtin_bit_cast(uint16_t, static_cast<__bf16>(acc[4 * e + 2] * inv)) |
+                   ((uint32_t)__builtin_bit_cast(uint16_t, static_cast<__bf16>(acc[4 * e + 3] * inv)) << 16);
+            *reinterpret_cast<uint2*>(orow + 4 * e) = pk;
+        }
+        if (lse != nullptr && t % TPR == 0)
+            lse[(size_t)bh * L + row] = wsum > 0.0f ? lmax + logf(wsum) : -INFINITY;
     }
 }
 
@@ -579,7 +705,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, const int32_t* __restrict__ kv_idx,
     const int32_t* __restrict__ kv_cnt, float scale, uint16_t* __restrict__ o,
-    float* __restrict__ lse, int L, int n, void* ws, int BH) {
+    float* __restrict__ lse, int L, int n, void* ws, int BH, int S) {
     constexpr int QW = BS / 32;        // waves per group = 32-row query slices of a block
     constexpr int NT = BS * 4;         // threads: two groups of QW waves
     constexpr int KVW = BS / 2;        // kv rows per unit (half a tile)
@@ -598,10 +724,11 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     __shared__ uint32_t ulist[kMaxBlocks];     // union of the two lists: j | membership << 16
     __shared__ uint8_t umask[kMaxBlocks];
     __shared__ int wsum[2 * NT / 64];
-    __shared__ int item_s;
+    __shared__ int item_s[4];          // pair, first step, end step, slot (-1: whole pair)
 
     // Persistent work-group on XCD blockIdx % 8 (dispatch order): items
-    // (head, pair of query blocks 2p, 2p+1) come from the plan.  Every
+    // (head, pair of query blocks 2p, 2p+1, or a chunk of the walk of a
+    // split pair) come from the plan.  Every
     // per-item value is derived inside the loop from copies of the thread
     // index and the workspace pointer that the compiler cannot see through,
     // so nothing is hoisted out of the loop to stay live in registers.
@@ -610,12 +737,29 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     void* wsi = ws;
     asm volatile("" : "+v"(tid));
     asm volatile("" : "+s"(wsi));
-    if (tid == 0) item_s = fetch_item(Plan(wsi, BH), blockIdx.x % kXcds);
-    __syncthreads();
-    const int item = item_s;
-    __syncthreads();   // item_s is rewritten only after every wave has read it
-    if (item < 0) break;
     const int npairs = (n + 1) / 2;
+    if (tid == 0) {
+        const Plan pl(wsi, BH, npairs, S);
+        const int it = fetch_item(pl, blockIdx.x % kXcds);
+        int4 desc = make_int4(it, 0, 0x7fffffff, -1);
+        if (it >= 0 && (it & kChunkBit)) {
+            const int k2 = it & (kChunkBit - 1);
+            desc = k2 < S ? pl.chunks[k2] : make_int4(-2, 0, 0, 0);
+            desc.w = k2;
+        }
+        // an item outside the plan's range is skipped (never read past the lists)
+        if (desc.x >= 0 && (long long)desc.x >= (long long)BH * npairs) desc.x = -2;
+        item_s[0] = desc.x;
+        item_s[1] = desc.y;
+        item_s[2] = desc.z;
+        item_s[3] = desc.w;
+    }
+    __syncthreads();
+    const int item = item_s[0];
+    const int step0 = item_s[1], step1 = item_s[2], slot = item_s[3];
+    __syncthreads();   // item_s is rewritten only after every wave has read it
+    if (item == -1) break;
+    if (item < 0) continue;
     const int bh = item / npairs, pr = item % npairs;
     const int lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
@@ -842,11 +986,15 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     // waits for it at the end of the tile (slot 4t+3); group 1 copies V(t+1)
     // into vp (last read in slot 4t+1) and waits for it at the end of its
     // next M phase (slot 4t+5).
-    uint32_t e_cur = ns > 0 ? ulist[0] : 0u;
-    uint32_t e_nxt = ns > 1 ? ulist[1] : 0u;
+    // The walk of the pair has max(cnt(2p), cnt(2p+1)) = ns + max(na, nb)
+    // steps: tiles 0 .. ns-1 of the shared part, then the slots of the
+    // exclusive part.  A chunk item walks steps [step0, step1) only.
+    const int t0 = min(step0, ns), t1 = min(step1, ns);
+    uint32_t e_cur = t0 < t1 ? ulist[t0] : 0u;
+    uint32_t e_nxt = t0 + 1 < t1 ? ulist[t0 + 1] : 0u;
     e_cur = __builtin_amdgcn_readfirstlane(e_cur);
     e_nxt = __builtin_amdgcn_readfirstlane(e_nxt);
-    if (ns > 0) copy.issue_all(g == 0 ? kg : vg, (int)(e_cur & 0xFFFF), L, g == 0 ? kb0 : vb0, qw, lane);
+    if (t0 < t1) copy.issue_all(g == 0 ? kg : vg, (int)(e_cur & 0xFFFF), L, g == 0 ? kb0 : vb0, qw, lane);
     // Q and the first tile are complete before the tile loop: no wait on
     // the memory counter (which also counts the tile copies) is left for the
     // loop to inherit.
@@ -860,7 +1008,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     // Every block of this part is in both lists: both groups run every phase
     // (the first product multiplies P = 0).
     auto tile = [&](int t, char* kc, char* kn, char* vc, char* vp) __attribute__((always_inline)) {
-        const bool more = t + 1 < ns;
+        const bool more = t + 1 < t1;
         const int jc = (int)(e_cur & 0xFFFF), jn = (int)(e_nxt & 0xFFFF);
         const int kvalid = min(BS, L - jc * BS);
         // first half: S from K(t) rows [0, KVW); product of V(t-1) rows [KVW, BS)
@@ -876,7 +1024,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
         // second half: S from K(t) rows [KVW, BS); product of V(t) rows [0, KVW)
         mphase(kc + HALF, vc, yes{});
         barrier();
-        uint32_t e_after = t + 2 < ns ? ulist[t + 2] : 0u;
+        uint32_t e_after = t + 2 < t1 ? ulist[t + 2] : 0u;
         e_after = __builtin_amdgcn_readfirstlane(e_after);
         xphase(kvalid, std::integral_constant<int, 1>{}, false, no_copy);
         if (g == 0) wait_copies();
@@ -890,7 +1038,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     char* kn = kb1;
     char* vc = vb0;
     char* vp = vb1;
-    for (int t = 0; t < ns; ++t) {
+    for (int t = t0; t < t1; ++t) {
         tile(t, kc, kn, vc, vp);
         char* tmp = kc;
         kc = kn;
@@ -900,7 +1048,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
         vp = tmp;
     }
     // the pending product of the last tile's second half (its V now in vp)
-    if (ns > 0) mphase(kc, vp + HALF, yes{});
+    if (t1 > t0) mphase(kc, vp + HALF, yes{});
     if (g == 0) barrier();   // both groups pass the same number of barriers
 
     // ---- blocks in one list only: both groups at once ----
@@ -913,19 +1061,20 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     // second unit, K(x+1) rows [KVW, BS) and V(x+1) rows [0, KVW).  A group
     // waits for its copies at the end of its next X phase.
     const int ce = max(na, nb);   // work-group uniform
-    if (ce > 0) {
+    const int x0 = min(ce, max(0, step0 - ns)), x1 = min(ce, max(0, step1 - ns));
+    if (x1 > x0) {
         barrier();   // group 1's last product of the shared part has read its buffers
-        const int cgx = g == 0 ? na : nb;
+        const int cgx = min(g == 0 ? na : nb, x1);   // this group's end of the walk
         const uint32_t* el = ulist + (g == 0 ? ns : ns + na);
         char* kbuf = g == 0 ? kb0 : kb1;
         char* vbuf = g == 0 ? vb0 : vb1;
         constexpr int IPH = Copy::IPH;
         zero_p();
-        uint32_t ec = cgx > 0 ? el[0] : 0u;
-        uint32_t en = cgx > 1 ? el[1] : 0u;
+        uint32_t ec = x0 < cgx ? el[x0] : 0u;
+        uint32_t en = x0 + 1 < cgx ? el[x0 + 1] : 0u;
         ec = __builtin_amdgcn_readfirstlane(ec);
         en = __builtin_amdgcn_readfirstlane(en);
-        if (cgx > 0) {
+        if (x0 < cgx) {
             // the first product multiplies P = 0 with this half: zeros, not stale LDS
             for (int e = 64 * qw + lane; e < HALF / 16; e += 64 * QW)
                 reinterpret_cast<uint4*>(vbuf + HALF)[e] = make_uint4(0, 0, 0, 0);
@@ -976,7 +1125,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
             else
                 wait_vmcnt<2 * IPH>();
         };
-        for (int x = 0; x < ce; ++x) {
+        for (int x = x0; x < x1; ++x) {
             const bool active = x < cgx;
             const bool more = x + 1 < cgx;
             const int jc = (int)(ec & 0xFFFF), jn = (int)(en & 0xFFFF);
@@ -1005,7 +1154,20 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
 
     // ---- output: this wave owns 32 complete query rows ----
     l += __shfl_xor(l, 32);
-    if (i < n && qrow < L) {
+    if (i < n && qrow < L && slot >= 0) {
+        // a chunk of a split pair: O / l in fp32 and the chunk's LSE into its slot
+        const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+        float* sl = Plan(wsi, BH, npairs, S).part + (size_t)slot * slot_floats(D, BS);
+        float* prow = sl + ((size_t)g * BS + 32 * qw + l32) * D;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int gq = 0; gq < 4; ++gq)
+                *reinterpret_cast<float4*>(prow + 32 * dt + 8 * gq + 4 * h) =
+                    make_float4(oacc[dt][4 * gq] * inv, oacc[dt][4 * gq + 1] * inv, oacc[dt][4 * gq + 2] * inv,
+                                oacc[dt][4 * gq + 3] * inv);
+        if (h == 0) sl[2 * BS * D + g * BS + 32 * qw + l32] = l > 0.0f ? m * scale + logf(l) : -INFINITY;
+    } else if (i < n && qrow < L) {
         const float inv = l > 0.0f ? 1.0f / l : 0.0f;
         uint16_t* orow = o + base + (size_t)qrow * D;
 #pragma unroll
@@ -1046,15 +1208,16 @@ int persistent_groups() {
 template <int D, int BS>
 hipError_t launch(const uint16_t* q, const uint16_t* k, const uint16_t* v, const int32_t* kv_idx,
                   const int32_t* kv_cnt, float scale, uint16_t* o, float* lse, int BH, int L, int n,
-                  void* ws, hipStream_t s) {
-    hipLaunchKernelGGL(plan_split_kernel, dim3((unsigned)BH), dim3(kPlanThreads), 0, s, kv_cnt, ws, BH, n);
-    hipLaunchKernelGGL(plan_order_kernel, dim3((unsigned)((BH + kPlanThreads - 1) / kPlanThreads)),
-                       dim3(kPlanThreads), 0, s, ws, BH);
-    hipLaunchKernelGGL(plan_lists_kernel, dim3(kXcds), dim3(kPlanThreads), 0, s, kv_cnt, ws, BH, n);
-    const long items = (long)BH * ((n + 1) / 2);
-    const unsigned groups = (unsigned)std::min<long>(persistent_groups(), items);
+                  void* ws, int S, hipStream_t s) {
+    const int ncu = persistent_groups();
+    hipLaunchKernelGGL(plan_kernel, dim3(kXcds), dim3(kPlanThreads), 0, s, kv_cnt, ws, BH, n, ncu, S);
+    const long items = (long)BH * ((n + 1) / 2) + S;
+    const unsigned groups = (unsigned)std::min<long>(ncu, items);
     hipLaunchKernelGGL((attn_fwd_kernel<D, BS>), dim3(groups), dim3(BS * 4), 0, s,
-                       q, k, v, kv_idx, kv_cnt, scale, o, lse, L, n, ws, BH);
+                       q, k, v, kv_idx, kv_cnt, scale, o, lse, L, n, ws, BH, S);
+    if (S > 0)
+        hipLaunchKernelGGL((merge_kernel<D, BS>), dim3((unsigned)(2 * ncu)), dim3(256), 0, s, ws, BH, n, S, L, o,
+                           lse);
     return hipGetLastError();
 }
 
@@ -1226,19 +1389,43 @@ hipError_t noalloc_scratch(void** out) {
     return hipSuccess;
 }
 
-size_t attn_workspace_bytes(int BH, int n) {
-    const size_t ints = (size_t)kPlanHdr + (size_t)BH * (11 + (size_t)(n + 1) / 2);
-    return (ints * sizeof(int) + 255) / 256 * 256;
+size_t attn_plan_bytes(int BH, int n, int S) {
+    return Plan::ints(BH, (n + 1) / 2, S) * sizeof(int);
+}
+
+size_t attn_slot_bytes(int d, int bs) { return slot_floats(d, bs) * sizeof(float); }
+
+int attn_max_slots(int BH, int n) {
+    // every chunk is at least kMinChunkSteps steps of a walk of at most n
+    const long long per_pair = (n + kMinChunkSteps - 1) / kMinChunkSteps;
+    const long long bound = per_pair > 1 ? (long long)BH * ((n + 1) / 2) * per_pair : 0;
+    return (int)std::min<long long>(kMaxSplitSlots, bound);
+}
+
+size_t attn_workspace_bytes(int BH, int n, int d, int bs) {
+    const int S = attn_max_slots(BH, n);
+    return attn_plan_bytes(BH, n, S) + (size_t)S * attn_slot_bytes(d, bs);
+}
+
+int attn_slots_for(int BH, int n, int d, int bs, size_t ws_bytes) {
+    const size_t base = attn_plan_bytes(BH, n, 0);
+    if (ws_bytes <= base) return 0;
+    // each slot adds 9 plan ints (item, chunk, split descriptors) and a slot
+    long long S = (long long)((ws_bytes - base) / (attn_slot_bytes(d, bs) + 9 * sizeof(int)));
+    S = std::min<long long>(S, attn_max_slots(BH, n));
+    while (S > 0 && attn_plan_bytes(BH, n, (int)S) + (size_t)S * attn_slot_bytes(d, bs) > ws_bytes) --S;
+    return S < 2 ? 0 : (int)S;
 }
 
 hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                            const int32_t* kv_idx, const int32_t* kv_cnt, float scale,
                            uint16_t* o, float* lse, int BH, int L, int d, int bs, int n,
-                           void* ws, hipStream_t s) {
-    if (d == 128 && bs == 128) return launch<128, 128>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, ws, s);
-    if (d == 128 && bs == 64) return launch<128, 64>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, ws, s);
-    if (d == 64 && bs == 128) return launch<64, 128>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, ws, s);
-    return launch<64, 64>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, ws, s);
+                           void* ws, size_t ws_bytes, hipStream_t s) {
+    const int S = attn_slots_for(BH, n, d, bs, ws_bytes);
+    if (d == 128 && bs == 128) return launch<128, 128>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, ws, S, s);
+    if (d == 128 && bs == 64) return launch<128, 64>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, ws, S, s);
+    if (d == 64 && bs == 128) return launch<64, 128>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, ws, S, s);
+    return launch<64, 64>(q, k, v, kv_idx, kv_cnt, scale, o, lse, BH, L, n, ws, S, s);
 }
 
 hipError_t launch_stat_count(const uint16_t* q, const uint16_t* k, const int32_t* kv_idx,

@@ -493,7 +493,13 @@ mod_status mod_predict_block_mask(mod_stats* s, const void* q, const void* k, in
 
 size_t mod_attn_workspace_bytes(const mod_shape* shape) {
     if (check_shape(shape, false) != MOD_OK) return 0;
-    return moddit::attn_workspace_bytes(shape->B * shape->H, ceil_div(shape->L, shape->block));
+    return moddit::attn_workspace_bytes(shape->B * shape->H, ceil_div(shape->L, shape->block), shape->d,
+                                        shape->block);
+}
+
+size_t mod_attn_plan_bytes(const mod_shape* shape) {
+    if (check_shape(shape, false) != MOD_OK) return 0;
+    return moddit::attn_plan_bytes(shape->B * shape->H, ceil_div(shape->L, shape->block), 0);
 }
 
 mod_status mod_block_sparse_attn_fwd(const mod_shape* shape, const void* q, const void* k,
@@ -504,9 +510,9 @@ mod_status mod_block_sparse_attn_fwd(const mod_shape* shape, const void* q, cons
     if (st != MOD_OK) return st;
     if (!q || !k || !v || !o || !kv_idx || !kv_cnt)
         return fail(MOD_ERR_INVALID_ARG, "q, k, v, o, kv_idx and kv_cnt must not be NULL");
-    const size_t need = moddit::attn_workspace_bytes(shape->B * shape->H, ceil_div(shape->L, shape->block));
+    const size_t need = moddit::attn_plan_bytes(shape->B * shape->H, ceil_div(shape->L, shape->block), 0);
     if (!workspace || ws_bytes < need)
-        return fail(MOD_ERR_INVALID_ARG, "workspace of %zu bytes needed (got %zu%s)", need, ws_bytes,
+        return fail(MOD_ERR_INVALID_ARG, "workspace of at least %zu bytes needed (got %zu%s)", need, ws_bytes,
                     workspace ? "" : ", NULL");
     if (reinterpret_cast<uintptr_t>(workspace) % 16 != 0)
         return fail(MOD_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
@@ -517,7 +523,7 @@ mod_status mod_block_sparse_attn_fwd(const mod_shape* shape, const void* q, cons
     hipError_t e = moddit::launch_attn_fwd(
         static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
         kv_idx, kv_cnt, sc, static_cast<uint16_t*>(o), lse, shape->B * shape->H, shape->L, shape->d,
-        shape->block, n, workspace, static_cast<hipStream_t>(stream));
+        shape->block, n, workspace, ws_bytes, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "attention launch");
     return MOD_OK;
 }
@@ -528,11 +534,12 @@ mod_status mod_block_sparse_attn_fwd_noalloc(const mod_shape* shape, const void*
                                              void* stream) {
     mod_status st = check_shape(shape, false);
     if (st != MOD_OK) return st;
-    const size_t need = moddit::attn_workspace_bytes(shape->B * shape->H, ceil_div(shape->L, shape->block));
+    // the work plan only: the no-allocation path does not split walks
+    const size_t need = moddit::attn_plan_bytes(shape->B * shape->H, ceil_div(shape->L, shape->block), 0);
     if (need > (size_t)MOD_ATTN_NOALLOC_MAX_BYTES)
         return fail(MOD_ERR_UNSUPPORTED,
                     "work plan of %zu bytes exceeds the %zu-byte library array of the no-allocation "
-                    "entry point (B*H*(11 + ceil(n/2)) too large); use mod_block_sparse_attn_fwd",
+                    "entry point (B*H*(ceil(n/2) + 16) too large); use mod_block_sparse_attn_fwd",
                     need, (size_t)MOD_ATTN_NOALLOC_MAX_BYTES);
     static_assert(moddit::kNoAllocScratchBytes == (size_t)MOD_ATTN_NOALLOC_MAX_BYTES,
                   "header and library disagree on the scratch size");

@@ -55,13 +55,17 @@ hipError_t launch_select_patterns(const double* pred, const int32_t* gate, const
                                   const int* row_hi, int K, uint8_t* chosen, int32_t* kv_idx,
                                   int32_t* kv_cnt, int BH, int n, int ldn, int tb0, hipStream_t s);
 
-// a6: block-sparse attention forward.  ws: device workspace of
-// attn_workspace_bytes(BH, n) bytes (the work plan, rewritten every call).
-size_t attn_workspace_bytes(int BH, int n);
+// a6: block-sparse attention forward.  ws: device workspace of ws_bytes
+// bytes, at least attn_plan_bytes(BH, n, 0) (the work plan, rewritten every
+// call); attn_workspace_bytes(BH, n, d, bs) also holds the partial results
+// of the split-KV path (split pairs need ws_bytes to hold >= 2 slots).
+size_t attn_plan_bytes(int BH, int n, int S);
+size_t attn_workspace_bytes(int BH, int n, int d, int bs);
+int attn_slots_for(int BH, int n, int d, int bs, size_t ws_bytes);
 hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                            const int32_t* kv_idx, const int32_t* kv_cnt, float scale,
                            uint16_t* o, float* lse, int BH, int L, int d, int bs, int n,
-                           void* ws, hipStream_t s);
+                           void* ws, size_t ws_bytes, hipStream_t s);
 
 // The attention's work plan in a library-owned device array of
 // kNoAllocScratchBytes per device (for callers that cannot allocate):

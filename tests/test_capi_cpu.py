@@ -97,12 +97,21 @@ def test_attention_rejects_null_pointers_on_host(M):
 
 
 def test_workspace_size(M):
-    """The attention workspace holds the work plan: one int per (head, pair of
-    query blocks) plus per-head tables; 0 for an invalid shape."""
-    ws = M.mod_attn_workspace_bytes(M.make_shape(1, 24, 118800, 128, 128, 3600))
-    assert ws >= 4 * 24 * 465 and ws % 256 == 0 and ws < 64 * 1024
-    assert M.mod_attn_workspace_bytes(M.make_shape(1, 2, 1024, 96, 64, 256)) == 0
-    assert M.mod_attn_workspace_bytes(None) == 0
+    """The attention workspace holds the work plan (one int per (head, pair of
+    query blocks) plus per-head tables) and, for walks longer than one
+    64-step chunk, up to 1024 partial-result slots of 8 * block * (d + 1)
+    bytes for the split-KV path; the plan alone is the minimum.  0 for an
+    invalid shape."""
+    hy = M.make_shape(1, 24, 118800, 128, 128, 3600)
+    plan = M.mod_attn_plan_bytes(hy)
+    assert plan >= 4 * 24 * 465 and plan % 256 == 0 and plan < 64 * 1024
+    ws = M.mod_attn_workspace_bytes(hy)
+    slot = 8 * 128 * 129
+    assert 1024 * slot + plan <= ws <= 1024 * (slot + 64) + plan
+    tiny = M.make_shape(1, 2, 1024, 64, 64, 256)           # n = 16: never split
+    assert M.mod_attn_workspace_bytes(tiny) == M.mod_attn_plan_bytes(tiny)
+    for bad in (M.make_shape(1, 2, 1024, 96, 64, 256), None):
+        assert M.mod_attn_workspace_bytes(bad) == 0 and M.mod_attn_plan_bytes(bad) == 0
 
 
 def test_struct_layouts_match_the_header(M, tmp_path):

@@ -440,3 +440,78 @@ def test_schedule_with_drift(rule):
     _, t1 = M.mod_stats_get_anchor(st.handle, 1, cfg.B, cfg.H, st.p)
     assert (t1, t2) == tuple(anchors[-2:])
     st.close()
+
+
+# ---------------------------------------------------------------- split-KV
+
+# Few pairs with long walks, so the work plan splits them: one 128-block
+# head of 300 blocks (ragged tail), two 64-token-block heads of 250 blocks.
+SPLIT_CASES = [(128, 128, 300 * 128 - 37, 1, 11), (64, 64, 250 * 64 - 10, 2, 12)]
+PLAN_MISC_INT = 8 * 32 + 16     # int offset of the plan's counters: [0] split pairs, [1] chunk steps
+
+
+def _uneven_lists(B, H, n, seed):
+    """Rows of every length: full rows, long and short random lists, empty
+    rows, neighbours of very different lengths (long one-list parts)."""
+    rng = np.random.default_rng(seed)
+    rows = [[None] * H for _ in range(B)]
+    idx = np.zeros((B, H, n, n), np.int32)
+    cnt = np.zeros((B, H, n), np.int32)
+    for b in range(B):
+        for h in range(H):
+            r = []
+            for i in range(n):
+                kind = rng.integers(0, 6)
+                m = {0: n, 1: 0, 2: int(rng.integers(1, 8))}.get(int(kind), int(rng.integers(n // 3, n)))
+                js = np.sort(rng.choice(n, size=m, replace=False)).astype(np.int32)
+                idx[b, h, i, :m] = js
+                cnt[b, h, i] = m
+                r.append(js.tolist())
+            rows[b][h] = r
+    return rows, torch.from_numpy(idx).cuda(), torch.from_numpy(cnt).cuda()
+
+
+@pytest.mark.parametrize("d,bs,L,H,seed", SPLIT_CASES)
+def test_attention_split_kv(d, bs, L, H, seed):
+    """Walks split into chunks whose fp32 partial results are merged in chunk
+    order: every query block against the oracle, deterministic over repeated
+    runs, and within tolerance of the unsplit run (plan-only workspace)."""
+    B = 1
+    n = -(-L // bs)
+    rng = np.random.default_rng(seed)
+    host = [W.to_bf16_bits(rng.standard_normal((B, H, L, d)).astype(np.float32) * (1.5 if t < 2 else 1.0))
+            for t in range(3)]
+    qd, kd, vd = (bf16_tensor(x) for x in host)
+    rows, idx, cnt = _uneven_lists(B, H, n, seed)
+    shape = M.make_shape(B, H, L, d, bs)
+    full, plan = M.mod_attn_workspace_bytes(shape), M.mod_attn_plan_bytes(shape)
+    assert full > plan
+    print(f"split-KV case d={d} block={bs} L={L} H={H} n={n}", flush=True)
+
+    def run(ws_bytes):
+        ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
+        o = torch.full_like(qd, float("nan"))
+        lse = torch.full((B, H, L), float("nan"), dtype=torch.float32, device="cuda")
+        M.mod_block_sparse_attn_fwd(shape, qd, kd, vd, idx, cnt, 0.0, o, lse, ws, ws_bytes)
+        torch.cuda.synchronize()
+        misc = ws[:4 * (PLAN_MISC_INT + 2)].view(torch.int32)[PLAN_MISC_INT:].cpu().tolist()
+        return o, lse, misc
+
+    o1, l1, misc = run(full)
+    assert misc[0] > 0 and misc[1] >= 64, misc          # pairs were split, chunks >= 64 steps
+    o2, l2, _ = run(full)
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)) and torch.equal(l1, l2)
+    o3, l3, misc3 = run(plan)
+    assert misc3[0] == 0
+    scale = 1.0 / math.sqrt(d)
+    for h in range(H):
+        qf, kf, vf = (W.bf16_bits_to_f64(x[0, h]) for x in host)
+        Oo, Lo = O.attention(qf, kf, vf, rows[0][h], bs, scale)
+        for og, lg in ((bf16_to_f64(o1[0, h]), l1[0, h]), (bf16_to_f64(o3[0, h]), l3[0, h])):
+            lg = lg.cpu().numpy().astype(np.float64)
+            mx, mean = attention_errors(og, Oo)
+            assert mx <= MAX_ABS and mean <= MEAN_ABS, (h, mx, mean)
+            fin = np.isfinite(Lo)
+            assert (np.isneginf(lg) == ~fin).all()
+            assert np.abs(lg[fin] - Lo[fin]).max() <= LSE_ABS
+    print(f"  {misc[0]} split pairs, chunks of {misc[1]} steps", flush=True)

@@ -111,9 +111,14 @@ CONFIGS = {
 
 
 def with_heads(cfg: LayerConfig, H: int, name: str | None = None) -> LayerConfig:
-    """The same layer with H heads (heads keep their seeds and types)."""
+    """The layer's first H heads (each keeps its seed and type: the types of
+    the whole layer are fixed explicitly, since the seeded draw depends on
+    the head count)."""
+    if not 1 <= H <= cfg.H:
+        raise ValueError(f"with_heads keeps 1..{cfg.H} heads, got {H}")
+    types = tuple(int(t) for t in head_types(cfg))
     return LayerConfig(name or cfg.name, cfg.B, H, cfg.d, cfg.frames, cfg.hs, cfg.ws,
-                       cfg.block, cfg.seed, cfg.head_types, cfg.text_tokens)
+                       cfg.block, cfg.seed, types, cfg.text_tokens)
 
 
 def with_text(cfg: LayerConfig, text_tokens: int, name: str | None = None) -> LayerConfig:
