@@ -420,9 +420,10 @@ def run_sweep(args):
                       "marginal_tflops": round(1e3 / float(b), 1)}), flush=True)
 
 
-def _layer_attention(M, W, cfg, mode, val, args, dev):
+def _layer_attention(M, W, cfg, mode, val, args, dev, plan_only=False):
     """Predicted lists (re-anchor step) and the attention's median time on
-    one layer; returns (attn_ms, kept flop per head)."""
+    one layer; returns (attn_ms, kept flop per head, attn_ms with a
+    plan-only workspace (no split walks) or None)."""
     import numpy as np
     import torch
     host = W.generate(cfg)
@@ -446,10 +447,19 @@ def _layer_attention(M, W, cfg, mode, val, args, dev):
     for _ in range(args.warmup):
         attn()
     attn_ms = _median_ms(attn, max(args.steps, 5), stream)
+    unsplit_ms = None
+    if plan_only:
+        pb = M.mod_attn_plan_bytes(shape)
+        attn_u = lambda: M.mod_block_sparse_attn_fwd(shape, qd, kd, vd, kv_idx, kv_cnt, 0.0, out,  # noqa: E731
+                                                     None, ws, pb, stream)
+        for _ in range(args.warmup):
+            attn_u()
+        unsplit_ms = _median_ms(attn_u, max(args.steps, 5), stream)
+        attn_ms = min(attn_ms, _median_ms(attn, max(args.steps, 5), stream))  # interleaved re-take
     per_head = np.array([kept_flops(kv_idx[:, h:h + 1], kv_cnt[:, h:h + 1], cfg.L, cfg.block, cfg.d)
                          for h in range(cfg.H)])
     st.close()
-    return attn_ms, per_head
+    return attn_ms, per_head, unsplit_ms
 
 
 def run_share(args):
@@ -466,11 +476,14 @@ def run_share(args):
     import workloads as W
 
     dev = torch.device("cuda:0")
-    for base, H in (("hunyuan", 3), ("wan", 5)):
+    layers = {}
+    for base, H in (("hunyuan", 3), ("wan", 5), ("hunyuan", 1)):
         full = W.CONFIGS[base]
-        t_full, w_full = _layer_attention(M, W, full, "mass", 0.75, args, dev)
+        if base not in layers:
+            layers[base] = _layer_attention(M, W, full, "mass", 0.75, args, dev)[:2]
+        t_full, w_full = layers[base]
         share = W.with_heads(full, H)
-        t_share, w_share = _layer_attention(M, W, share, "mass", 0.75, args, dev)
+        t_share, w_share, t_unsplit = _layer_attention(M, W, share, "mass", 0.75, args, dev, plan_only=True)
         assert np.allclose(w_share, w_full[:H])       # the share's heads are the layer's first H
         ideal = t_full * w_share.sum() / w_full.sum()
         print(json.dumps({
@@ -485,6 +498,8 @@ def run_share(args):
             "layer_attn_ms": round(t_full, 3),
             "layer_attn_tflops": round(float(w_full.sum()) / (t_full * 1e-3) / 1e12, 1),
             "makespan_vs_ideal": round(t_share / ideal, 3),
+            "share_attn_ms_unsplit": round(t_unsplit, 3),
+            "makespan_vs_ideal_unsplit": round(t_unsplit / ideal, 3),
         }), flush=True)
 
 
