@@ -62,6 +62,21 @@ __device__ __forceinline__ float max_across_halves(float x) {
     return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
+// Sum of an int over the 64 lanes of a wave (every lane receives it) with
+// DPP moves only (no LDS traffic): pairs, quads, half rows and rows by lane
+// permutations, then rows 1 and 3 add the row before them (row_bcast:15)
+// and rows 2 and 3 add lane 31 (row_bcast:31), which leaves the total in
+// lane 63.
+__device__ __forceinline__ int wave_sum(int x) {
+    x += __builtin_amdgcn_update_dpp(0, x, 0xb1, 0xf, 0xf, false);    // quad_perm [1,0,3,2]
+    x += __builtin_amdgcn_update_dpp(0, x, 0x4e, 0xf, 0xf, false);    // quad_perm [2,3,0,1]
+    x += __builtin_amdgcn_update_dpp(0, x, 0x141, 0xf, 0xf, false);   // row_half_mirror
+    x += __builtin_amdgcn_update_dpp(0, x, 0x140, 0xf, 0xf, false);   // row_mirror
+    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);   // row_bcast:15 into rows 1, 3
+    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);   // row_bcast:31 into rows 2, 3
+    return __builtin_amdgcn_readlane(x, 63);
+}
+
 // Direct-to-LDS copy of 16 bytes per lane: lane l writes LDS bytes
 // [lds + 16 l, +16) with the 16 bytes at sbase + voff (sbase wave-uniform,
 // voff the lane's byte offset).  Written as inline assembly so that the
@@ -250,6 +265,7 @@ constexpr int kPlanBuckets = 512;
 constexpr int kChunkBit = 1 << 30;    // item flag: a chunk of a split pair (slot in the low bits)
 constexpr int kMinChunkSteps = 64;    // shortest chunk of a split walk
 constexpr int kMaxSplitSlots = 1024;  // partial-result slots a workspace holds at most
+constexpr int kPlanCache = 16384;     // pairs whose counts the plan keeps in LDS
 
 // Work-plan layout in the workspace (ints, then the partial-result slots).
 struct Plan {
@@ -313,6 +329,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const int32_t* __res
                                                             int BH, int n, int ncu, int S) {
     __shared__ long long scan64[kPlanThreads];
     __shared__ int xcnt[kXcds];
+    __shared__ uint32_t cache[kPlanCache];   // both counts of a pair, 16 bits each
     const int x = blockIdx.x, t = threadIdx.x;
     const int npairs = (n + 1) / 2;
     const long long P = (long long)BH * npairs;
@@ -321,10 +338,27 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const int32_t* __res
     const long long per = (P + kPlanThreads - 1) / kPlanThreads;
     const long long q0 = min(P, (long long)t * per), q1 = min(P, q0 + per);
     struct Pair { int c0, c1; };
-    auto counts = [&](long long q) {
+    auto load_counts = [&](long long q) {
         const int bh = (int)(q / npairs), p = (int)(q % npairs);
         const size_t r0 = (size_t)bh * n + 2 * p;
         return Pair{clamp_count(kv_cnt, r0, n), 2 * p + 1 < n ? clamp_count(kv_cnt, r0 + 1, n) : 0};
+    };
+    // every pass reads the counts: from LDS when they fit (loaded once,
+    // coalesced), else from the lists' counts in memory
+    const bool cached = P <= kPlanCache;
+    if (cached) {
+        for (long long q = t; q < P; q += kPlanThreads) {
+            const Pair c = load_counts(q);
+            cache[q] = (uint32_t)c.c0 | ((uint32_t)c.c1 << 16);
+        }
+        __syncthreads();
+    }
+    auto counts = [&](long long q) {
+        if (cached) {
+            const uint32_t v = cache[q];
+            return Pair{(int)(v & 0xFFFF), (int)(v >> 16)};
+        }
+        return load_counts(q);
     };
     // cost before every pair (global order) and before every head
     long long mine = 0;
@@ -1231,10 +1265,16 @@ hipError_t launch(const uint16_t* q, const uint16_t* k, const uint16_t* v, const
 // MFMA product.  Like the attention, one work-group per (head, pair of query
 // blocks 2p, 2p+1) walks the union of the two lists with two groups of BS/32
 // waves (32 query rows each), so every K tile copied into LDS serves both
-// blocks; K tiles are double-buffered and copied by all waves one tile ahead.
-// A lane counts its own products, the wave sums over lanes, and the
-// group's count of a tile is written into stat[bh][i][j] (fp64) after the
-// tile's barrier; blocks not listed keep their previous value (the
+// blocks (double-buffered, every wave copying its share of the next tile).
+// Per tile each wave computes S^T = K Q^T for its 32 query rows by MFMA and
+// counts its entries that reach the row's threshold (per lane, then summed
+// over the wave).  The groups are skewed by one tile with a single
+// work-group barrier per tile: in the interval of tile t group 0 multiplies
+// tile t and then counts it, while group 1 first counts tile t-1 (its scores
+// kept in registers) and then multiplies tile t, so on each SIMD one wave's
+// matrix products run beside the other wave's compares.  A group's count of
+// a tile is summed over its waves and written into stat[bh][i][j] (fp64)
+// after the next barrier; blocks not listed keep their previous value (the
 // reconstruction of Eq. 5).
 // With a text segment after the video the lists cover all n blocks of the
 // sequence while the statistic covers the first nv (video) blocks: rows
@@ -1252,12 +1292,12 @@ __global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
     constexpr int KK = D / 16;
     constexpr int TILE = BS * D * 2;
     constexpr int ROWB = 2 * D;
-    using Copy = TileCopy<D, BS, 2 * QW>;
+    using Copy = TileCopy<D, BS, 2 * QW>;   // copies by all waves
     __shared__ __align__(1024) char kbuf[2][TILE];   // K tiles, double-buffered
     __shared__ uint32_t ulist[kMaxBlocks];
     __shared__ uint8_t umask[kMaxBlocks];
     __shared__ int wsum[NT / 64];
-    __shared__ int part[2][2][QW];
+    __shared__ int part[2][2][QW];     // [tile parity][group][wave] counts
 
     const int npv = (nv + 1) / 2;      // pairs of video rows
     const int bh = blockIdx.x / npv, pr = blockIdx.x % npv;
@@ -1284,60 +1324,132 @@ __global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
     }
     // a row past the end of the sequence (or of the video rows) never counts
     const float thr = row_ok ? (lse[(size_t)bh * L + qrow] + log_eta) / scale : INFINITY;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) asm volatile("" : "+v"(qreg[kk]));
     __syncthreads();   // publishes the union list
 
     const Copy copy(lane);
     const uint16_t* kg = k + base;
     const int ka = l32 * ROWB + ((h ^ swz<D>(l32)) << 4);
-    // tile t+1 is copied while tile t is counted (its buffer was last read
-    // while counting tile t-1)
-    if (ucnt > 0) copy.issue_all(kg, (int)(ulist[0] & 0xFFFF), L, kbuf[0], w, lane);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    for (int t = 0; t < ucnt; ++t) {
-        const char* cur = kbuf[t & 1];
-        if (t + 1 < ucnt) copy.issue_all(kg, (int)(ulist[t + 1] & 0xFFFF), L, kbuf[(t + 1) & 1], w, lane);
-        const uint32_t e = __builtin_amdgcn_readfirstlane(ulist[t]);
-        const int j = (int)(e & 0xFFFF);
-        const bool member = ((e >> (16 + g)) & 1u) != 0;
-        const int kvalid = min(BS, L - j * BS);
-        int c = 0;
-        if (member) {
+
+    f32x16 sacc[RT];
+    // S^T of a whole tile: the RT sub-tiles' chains interleaved, operand
+    // loads PF steps ahead of their products (pinned step by step)
+    auto multiply = [&](const char* kt) __attribute__((always_inline)) {
+        constexpr int NS = RT * KK;
+        constexpr int PF = 6;
+        bf16x8 ak[NS];
+        auto load = [&](int s2) __attribute__((always_inline)) {
+            const int kk = s2 / RT, rt = s2 % RT;
+            ak[s2] = __builtin_bit_cast(bf16x8,
+                                        *reinterpret_cast<const uint4*>(kt + ((ka ^ (32 * kk)) + 32 * rt * ROWB)));
+        };
+#pragma unroll
+        for (int s2 = 0; s2 < PF; ++s2) load(s2);
+#pragma unroll
+        for (int s2 = 0; s2 < NS; ++s2) {
+            if (s2 + PF < NS) load(s2 + PF);
+            const int kk = s2 / RT, rt = s2 % RT;
+            sacc[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[s2], qreg[kk], kk == 0 ? f32x16{} : sacc[rt], 0, 0,
+                                                               0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    // entries of the tile in sacc that reach the row's threshold, summed over
+    // the wave; rows at or past kvalid (the end of the sequence, in a short
+    // tail tile only) are first set to -inf so that they never count
+    auto count = [&](int kvalid) __attribute__((always_inline)) {
+        if (kvalid < BS) {
+            asm volatile("" ::: "memory");
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt) {
-                f32x16 sv = f32x16{};
+                const int lim = kvalid - (32 * rt + 4 * h);
 #pragma unroll
-                for (int kk = 0; kk < KK; ++kk) {
-                    const bf16x8 a = __builtin_bit_cast(
-                        bf16x8, *reinterpret_cast<const uint4*>(cur + ((ka ^ (32 * kk)) + 32 * rt * ROWB)));
-                    sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sv, 0, 0, 0);
-                }
-                if (kvalid == BS) {
-#pragma unroll
-                    for (int ii = 0; ii < 16; ++ii) c += sv[ii] >= thr ? 1 : 0;
-                } else {
-                    // short tail tile: rows at or past the end of the sequence never count
-#pragma unroll
-                    for (int ii = 0; ii < 16; ++ii) {
-                        const int kv = 32 * rt + 8 * (ii >> 2) + 4 * h + (ii & 3);
-                        c += (kv < kvalid && sv[ii] >= thr) ? 1 : 0;
-                    }
-                }
+                for (int ii = 0; ii < 16; ++ii)
+                    sacc[rt][ii] = (8 * (ii >> 2) + (ii & 3) >= lim) ? -INFINITY : sacc[rt][ii];
             }
-#pragma unroll
-            for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
         }
-        if (lane == 0) part[t & 1][g][qw] = c;
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
-        if (member && qw == 0 && lane == 0 && i < nv && j < nv) {
+        int c = 0;
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int ii = 0; ii < 16; ++ii) c += sacc[rt][ii] >= thr ? 1 : 0;
+        return c;   // this lane's count; wave_sum() totals it
+    };
+    // the group's count of a finished tile, written by the group's first wave
+    auto flush = [&](int parity, int j, int kvalid) __attribute__((always_inline)) {
+        if (qw == 0 && lane == 0 && i < nv && j < nv) {
             int total = 0;
 #pragma unroll
-            for (int ww = 0; ww < QW; ++ww) total += part[t & 1][g][ww];
+            for (int ww = 0; ww < QW; ++ww) total += part[parity][g][ww];
             stat[((size_t)bh * nv + i) * nv + j] = (double)total / ((double)rows_i * (double)kvalid);
         }
+    };
+    auto entry = [&](int t) __attribute__((always_inline)) {
+        return __builtin_amdgcn_readfirstlane(ulist[t]);
+    };
+
+    if (ucnt > 0) copy.issue_all(kg, (int)(entry(0) & 0xFFFF), L, kbuf[0], w, lane);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) asm volatile("" : "+v"(qreg[kk]));
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    // interval t (t = 0 .. ucnt; group 0 idles in the last one): the next
+    // tile's copies, group 0 multiplies and counts tile t, group 1 counts
+    // tile t-1 and multiplies tile t; the counts of interval t-1 are flushed
+    for (int t = 0; t <= ucnt; ++t) {
+        if (t + 1 < ucnt) copy.issue_all(kg, (int)(entry(t + 1) & 0xFFFF), L, kbuf[(t + 1) & 1], w, lane);
+        const char* cur = kbuf[t & 1];
+        uint32_t ec = t < ucnt ? entry(t) : 0u;
+        const int jc = (int)(ec & 0xFFFF);
+        const bool mc = t < ucnt && ((ec >> (16 + g)) & 1u) != 0;
+        const int vc = min(BS, L - jc * BS);
+        if (t > 0) {
+            // flush of the previous interval's counts (group 0: tile t-1, group 1: tile t-2)
+            const int tf = g == 0 ? t - 1 : t - 2;
+            if (tf >= 0) {
+                const uint32_t ef = entry(tf);
+                const int jf = (int)(ef & 0xFFFF);
+                if (((ef >> (16 + g)) & 1u) != 0) flush(tf & 1, jf, min(BS, L - jf * BS));
+            }
+        }
+        if (g == 0) {
+            if (mc) {
+                __builtin_amdgcn_s_setprio(1);
+                multiply(cur);
+                __builtin_amdgcn_s_setprio(0);
+                const int c = wave_sum(count(vc));
+                if (lane == 0) part[t & 1][0][qw] = c;
+            }
+        } else {
+            // counts of tile t-1 per lane first (they free sacc), the wave's
+            // total after this tile's products are issued
+            int c = 0;
+            bool pm = false;
+            if (t > 0) {
+                const uint32_t ep = entry(t - 1);
+                const int jp = (int)(ep & 0xFFFF);
+                pm = ((ep >> 17) & 1u) != 0;
+                if (pm) c = count(min(BS, L - jp * BS));
+            }
+            if (mc) {
+                __builtin_amdgcn_s_setprio(1);
+                multiply(cur);
+                __builtin_amdgcn_s_setprio(0);
+            }
+            if (pm) {
+                c = wave_sum(c);
+                if (lane == 0) part[(t - 1) & 1][1][qw] = c;
+            }
+        }
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) asm volatile("" : "+v"(sacc[rt]));
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+    }
+    // group 1's count of the last tile (interval ucnt) is flushed here
+    if (g == 1 && ucnt > 0) {
+        const uint32_t ef = entry(ucnt - 1);
+        const int jf = (int)(ef & 0xFFFF);
+        if (((ef >> 17) & 1u) != 0) flush((ucnt - 1) & 1, jf, min(BS, L - jf * BS));
     }
 }
 

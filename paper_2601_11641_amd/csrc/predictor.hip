@@ -76,30 +76,50 @@ __device__ T block_exclusive_scan(T v, T* wsum, T* total) {
 
 // ---------------------------------------------------------------------------
 // a1: block pooling.  Grid (n, BH, 2): z = 0 pools Q, z = 1 pools K.  The
-// block is one contiguous run of rows*D bf16; each thread reads 16-byte
-// chunks of a fixed channel group on every R-th row and accumulates in fp64.
-// L: tokens pooled (the video tokens); L_stride: tokens per head in memory.
+// block is one contiguous run of rows*D bf16.  Lane l of wave w reads the
+// 16-byte chunk l % C (C = D / 8 chunks per row) of rows p*RPP + w*RPW +
+// l / C of every pass p; all of a thread's loads (non-temporal) are issued
+// before any is used (the whole 32 KB block in flight per work-group), and
+// accumulated in fp64.  The rows of a wave are then folded with lane shuffles (xor C, 2C,
+// ...), the four waves' sums through LDS in wave order: a fixed summation
+// order.  L: tokens pooled (the video tokens); L_stride: tokens per head in
+// memory.
 // ---------------------------------------------------------------------------
-template <int D>
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+template <int D, int BS>
 __global__ __launch_bounds__(kThreads) void pool_kernel(const uint16_t* __restrict__ q,
                                                         const uint16_t* __restrict__ k,
                                                         double* __restrict__ qbar,
                                                         double* __restrict__ kbar, int L,
-                                                        int L_stride, int bs, int n) {
-    constexpr int C = D / 8;        // 16-byte chunks per row
-    constexpr int R = kThreads / C; // rows per pass
-    __shared__ double part[R][D + 1];
+                                                        int L_stride, int n) {
+    constexpr int C = D / 8;               // 16-byte chunks per row
+    constexpr int NW = kThreads / 64;      // waves
+    constexpr int RPW = 64 / C;            // rows per wave per pass
+    constexpr int RPP = NW * RPW;          // rows per pass
+    constexpr int NP = BS / RPP;           // passes
+    static_assert(BS % RPP == 0, "block rows must fill whole passes");
+    __shared__ double part[NW][D];
     const int i = blockIdx.x, bh = blockIdx.y;
-    const uint16_t* src = (blockIdx.z == 0 ? q : k) + ((size_t)bh * L_stride + (size_t)i * bs) * D;
+    const uint16_t* src = (blockIdx.z == 0 ? q : k) + ((size_t)bh * L_stride + (size_t)i * BS) * D;
     double* dst = (blockIdx.z == 0 ? qbar : kbar) + ((size_t)bh * n + i) * D;
-    const int cnt = min(bs, L - i * bs);
-    const int t = threadIdx.x, c = t % C, r0 = t / C;
+    const int cnt = min(BS, L - i * BS);
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6, c = lane % C, rs = lane / C;
+    uint4 v[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        const int r = p * RPP + w * RPW + rs;
+        // read once and never again: non-temporal loads keep the stream out of the caches
+        v[p] = r < cnt ? __builtin_bit_cast(uint4, __builtin_nontemporal_load(
+                             reinterpret_cast<const u32x4*>(src + (size_t)r * D + c * 8)))
+                       : make_uint4(0, 0, 0, 0);
+    }
     double acc[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[e] = 0.0;
-    for (int r = r0; r < cnt; r += R) {
-        const uint4 w = *reinterpret_cast<const uint4*>(src + (size_t)r * D + c * 8);
-        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        const uint32_t ws[4] = {v[p].x, v[p].y, v[p].z, v[p].w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             acc[2 * e] += bf16_bits_to_double(ws[e] & 0xFFFFu);
@@ -107,12 +127,19 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(const uint16_t* __restri
         }
     }
 #pragma unroll
-    for (int e = 0; e < 8; ++e) part[r0][c * 8 + e] = acc[e];
+    for (int off = C; off < 64; off <<= 1)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], off);
+    if (rs == 0) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) part[w][c * 8 + e] = acc[e];
+    }
     __syncthreads();
     if (t < D) {
-        double s = 0.0;
-        for (int r = 0; r < R; ++r) s += part[r][t];
-        dst[t] = s / static_cast<double>(cnt);
+        double sum = 0.0;
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) sum += part[ww][t];
+        dst[t] = sum / static_cast<double>(cnt);
     }
 }
 
@@ -965,10 +992,14 @@ __global__ __launch_bounds__(kThreads) void text_rows_kernel(int32_t* __restrict
 hipError_t launch_pool(const uint16_t* q, const uint16_t* k, double* qbar, double* kbar,
                        int BH, int L, int L_stride, int d, int bs, int n, hipStream_t s) {
     const dim3 grid(n, BH, 2);
-    if (d == 128)
-        hipLaunchKernelGGL(pool_kernel<128>, grid, dim3(kThreads), 0, s, q, k, qbar, kbar, L, L_stride, bs, n);
+    if (d == 128 && bs == 128)
+        hipLaunchKernelGGL((pool_kernel<128, 128>), grid, dim3(kThreads), 0, s, q, k, qbar, kbar, L, L_stride, n);
+    else if (d == 128)
+        hipLaunchKernelGGL((pool_kernel<128, 64>), grid, dim3(kThreads), 0, s, q, k, qbar, kbar, L, L_stride, n);
+    else if (bs == 128)
+        hipLaunchKernelGGL((pool_kernel<64, 128>), grid, dim3(kThreads), 0, s, q, k, qbar, kbar, L, L_stride, n);
     else
-        hipLaunchKernelGGL(pool_kernel<64>, grid, dim3(kThreads), 0, s, q, k, qbar, kbar, L, L_stride, bs, n);
+        hipLaunchKernelGGL((pool_kernel<64, 64>), grid, dim3(kThreads), 0, s, q, k, qbar, kbar, L, L_stride, n);
     return hipGetLastError();
 }
 
