@@ -29,6 +29,7 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 ATTN_SOURCE = os.path.join(ROOT, "paper_2601_11641_amd", "csrc", "attn_fwd.hip")
+PRED_SOURCE = os.path.join(ROOT, "paper_2601_11641_amd", "csrc", "predictor.hip")
 COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "attn_fwd_hunyuan720p_counters.json")
 
 # rocprofv3 counter passes behind COUNTER_SUMMARY (one run each, see that file)
@@ -115,9 +116,9 @@ def parse():
     return ap.parse_args()
 
 
-def source_digest() -> str:
+def source_digest(path: str = ATTN_SOURCE) -> str:
     import hashlib
-    with open(ATTN_SOURCE, "rb") as f:
+    with open(path, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
@@ -207,6 +208,7 @@ def summarize_counters(pmc_dir: str):
         "kernel": "attn_fwd_kernel<128, 128>",
         "workload": "hunyuan-720p layer, mass budget 0.75 (bench.py --steps 1 --warmup 0)",
         "attn_source_sha256_16": source_digest(),
+        "predictor_source_sha256_16": source_digest(PRED_SOURCE),
         "commands": [f"rocprofv3 --pmc {COUNTER_PASSES[p]} -d gpurun_out/pmc/{p} -o pmc "
                      f"--output-format csv -- python3 bench.py "
                      + ("--calibrate-copy" if p in "EF" else
@@ -259,6 +261,20 @@ def measured_traffic():
     if c.get("attn_source_sha256_16") != source_digest():
         return None
     return c.get("traffic_bytes")
+
+
+def measured_pool():
+    """The pooling kernel's HBM figures from the committed counter summary
+    (its duration under the profiler and the algorithmic bytes of the 720p
+    Hunyuan layer), or None when the predictor source has changed since."""
+    try:
+        with open(COUNTER_SUMMARY) as f:
+            c = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if c.get("predictor_source_sha256_16") != source_digest(PRED_SOURCE) or "pool_kernel" not in c:
+        return None
+    return c["pool_kernel"]
 
 
 def calibrate_copy():
@@ -738,6 +754,21 @@ def main():
             "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
             "traffic": measured_traffic() if args.workload == "hunyuan-720p" else None,
         },
+    }
+    # the predictor's HBM-bound kernel (block pooling: Q and K read once) against
+    # the HBM peak, from the committed rocprofv3 counter passes of this layer
+    pool = measured_pool() if args.workload == "hunyuan-720p" else None
+    line["predictor"] = {
+        "kernel": "pool_kernel",
+        "bound": "hbm",
+        "achieved": pool["algorithmic_GBps"] if pool else None,
+        "peak": PEAK_HBM_GBS,
+        "unit": "GB/s",
+        "frac": pool["frac_of_8TBps"] if pool else None,
+        "bytes": pool["algorithmic_bytes"] if pool else None,
+        "kernel_us": pool["duration_us_under_profiler"] if pool else None,
+        "predict_ms": round(pred_ms, 4),
+        "predict_share_of_step": round(pred_ms / ms_step, 4),
     }
     if not args.no_cpu_baseline:
         idx = kv_idx[0, 0].cpu().numpy()

@@ -14,7 +14,12 @@ at the same cumulative-mass budget, and reports per head
 Recall and SMFS are taken over all query blocks of the small layer and over
 a seeded sample of query blocks (including the last) at 720p.
 
+The warm-up is one dense step (one anchor; the inputs do not drift, so a
+second identical anchor would give the same zero-slope prediction).
+
 usage: python oracle/mask_quality.py {small|hunyuan|wan} [rows per head] > out.jsonl
+(at 720p, MALLOC_MMAP_MAX_=0 MALLOC_TRIM_THRESHOLD_=100000000000 keep the
+large per-block temporaries in the heap instead of mapping them afresh)
 """
 from __future__ import annotations
 
@@ -33,7 +38,7 @@ if ROOT not in sys.path:
 import oracle as O  # noqa: E402
 import workloads as W  # noqa: E402
 
-WARM = 5
+WARM = 1
 MASS = 0.75
 
 
@@ -53,15 +58,13 @@ def head_report(cfg, h, qf, kf, rows):
     full = [list(range(n))] * n
     # pooled statistic
     P0 = O.Predictor(1, 1, cfg.L, cfg.d, cfg.block, cfg.frame_tokens, warmup_m=WARM, delta_t=0)
-    P0.collect(qf, kf, WARM - 1)
     P0.collect(qf, kf, WARM)
     sel0 = P0.predict(qf, kf, WARM + 1, budget)[0][0]
     G = P0.pooled_mass(qf, kf)[0, 0]
     nae0 = O.nae(G, P0.anchors[-1][1][0, 0], P0.regions)
-    # the paper's statistic (Eq. 2 on the dense map, both warm-up anchors dense)
+    # the paper's statistic (Eq. 2 on the dense map of the warm-up step)
     P1 = O.Predictor(1, 1, cfg.L, cfg.d, cfg.block, cfg.frame_tokens, warmup_m=WARM, delta_t=0,
                      statistic="attention")
-    P1.update(qf, kf, [[full]], WARM - 1)
     P1.update(qf, kf, [[full]], WARM)
     sel1 = P1.predict(None, None, WARM + 1, budget)[0][0]
     nae1 = O.nae(P1.stat[0, 0], P1.anchors[-1][1][0, 0], P1.regions)
