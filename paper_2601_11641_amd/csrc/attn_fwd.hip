@@ -1274,8 +1274,9 @@ hipError_t launch(const uint16_t* q, const uint16_t* k, const uint16_t* v, const
 // kept in registers) and then multiplies tile t, so on each SIMD one wave's
 // matrix products run beside the other wave's compares.  A group's count of
 // a tile is summed over its waves and written into stat[bh][i][j] (fp64)
-// after the next barrier; blocks not listed keep their previous value (the
-// reconstruction of Eq. 5).
+// after the next barrier, by group 0's first wave at the end of its interval
+// (off group 1's path, which bounds the interval); blocks not listed keep
+// their previous value (the reconstruction of Eq. 5).
 // With a text segment after the video the lists cover all n blocks of the
 // sequence while the statistic covers the first nv (video) blocks: rows
 // i < nv are counted and only entries j < nv are stored (stat [BH, nv, nv]).
@@ -1309,7 +1310,6 @@ __global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
     const size_t base = (size_t)bh * L * D;
     const int qrow = i * BS + 32 * qw + l32;
     const bool row_ok = i < nv && qrow < L;
-    const int rows_i = min(BS, L - i * BS);
 
     const size_t row0 = (size_t)bh * n + 2 * pr;
     const int ucnt = union_of_rows<NT>(kv_idx, kv_cnt, row0, 2 * pr + 1 < nv, n, umask, ulist, wsum, tid,
@@ -1374,13 +1374,15 @@ __global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
             for (int ii = 0; ii < 16; ++ii) c += sacc[rt][ii] >= thr ? 1 : 0;
         return c;   // this lane's count; wave_sum() totals it
     };
-    // the group's count of a finished tile, written by the group's first wave
-    auto flush = [&](int parity, int j, int kvalid) __attribute__((always_inline)) {
-        if (qw == 0 && lane == 0 && i < nv && j < nv) {
+    // group gg's count of a finished tile (block 2p+gg, kv block j)
+    auto flush = [&](int gg, int parity, int j) __attribute__((always_inline)) {
+        const int ig = 2 * pr + gg;
+        if (lane == 0 && ig < nv && j < nv) {
             int total = 0;
 #pragma unroll
-            for (int ww = 0; ww < QW; ++ww) total += part[parity][g][ww];
-            stat[((size_t)bh * nv + i) * nv + j] = (double)total / ((double)rows_i * (double)kvalid);
+            for (int ww = 0; ww < QW; ++ww) total += part[parity][gg][ww];
+            stat[((size_t)bh * nv + ig) * nv + j] =
+                (double)total / ((double)min(BS, L - ig * BS) * (double)min(BS, L - j * BS));
         }
     };
     auto entry = [&](int t) __attribute__((always_inline)) {
@@ -1394,23 +1396,21 @@ __global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
     __syncthreads();
     // interval t (t = 0 .. ucnt; group 0 idles in the last one): the next
     // tile's copies, group 0 multiplies and counts tile t, group 1 counts
-    // tile t-1 and multiplies tile t; the counts of interval t-1 are flushed
+    // tile t-1 and multiplies tile t; group 0's first wave then flushes the
+    // counts of interval t-1 (group 0's tile t-1, group 1's tile t-2).  The
+    // list entries of tiles t-2 .. t+1 are carried in scalar registers; the
+    // entry of tile t+2 is read from LDS at the start of the interval and
+    // taken at its end.
+    uint32_t em2 = 0u, em1 = 0u;
+    uint32_t e0 = ucnt > 0 ? entry(0) : 0u;
+    uint32_t e1 = ucnt > 1 ? entry(1) : 0u;
     for (int t = 0; t <= ucnt; ++t) {
-        if (t + 1 < ucnt) copy.issue_all(kg, (int)(entry(t + 1) & 0xFFFF), L, kbuf[(t + 1) & 1], w, lane);
+        if (t + 1 < ucnt) copy.issue_all(kg, (int)(e1 & 0xFFFF), L, kbuf[(t + 1) & 1], w, lane);
+        const uint32_t e2v = ulist[min(t + 2, max(ucnt - 1, 0))];
         const char* cur = kbuf[t & 1];
-        uint32_t ec = t < ucnt ? entry(t) : 0u;
-        const int jc = (int)(ec & 0xFFFF);
-        const bool mc = t < ucnt && ((ec >> (16 + g)) & 1u) != 0;
+        const int jc = (int)(e0 & 0xFFFF);
+        const bool mc = t < ucnt && ((e0 >> (16 + g)) & 1u) != 0;
         const int vc = min(BS, L - jc * BS);
-        if (t > 0) {
-            // flush of the previous interval's counts (group 0: tile t-1, group 1: tile t-2)
-            const int tf = g == 0 ? t - 1 : t - 2;
-            if (tf >= 0) {
-                const uint32_t ef = entry(tf);
-                const int jf = (int)(ef & 0xFFFF);
-                if (((ef >> (16 + g)) & 1u) != 0) flush(tf & 1, jf, min(BS, L - jf * BS));
-            }
-        }
         if (g == 0) {
             if (mc) {
                 __builtin_amdgcn_s_setprio(1);
@@ -1419,17 +1419,16 @@ __global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
                 const int c = wave_sum(count(vc));
                 if (lane == 0) part[t & 1][0][qw] = c;
             }
+            if (qw == 0) {
+                if (t >= 1 && ((em1 >> 16) & 1u) != 0) flush(0, (t - 1) & 1, (int)(em1 & 0xFFFF));
+                if (t >= 2 && ((em2 >> 17) & 1u) != 0) flush(1, t & 1, (int)(em2 & 0xFFFF));
+            }
         } else {
             // counts of tile t-1 per lane first (they free sacc), the wave's
             // total after this tile's products are issued
             int c = 0;
-            bool pm = false;
-            if (t > 0) {
-                const uint32_t ep = entry(t - 1);
-                const int jp = (int)(ep & 0xFFFF);
-                pm = ((ep >> 17) & 1u) != 0;
-                if (pm) c = count(min(BS, L - jp * BS));
-            }
+            const bool pm = t > 0 && ((em1 >> 17) & 1u) != 0;
+            if (pm) c = count(min(BS, L - (int)(em1 & 0xFFFF) * BS));
             if (mc) {
                 __builtin_amdgcn_s_setprio(1);
                 multiply(cur);
@@ -1442,15 +1441,17 @@ __global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
         }
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) asm volatile("" : "+v"(sacc[rt]));
+        const uint32_t e2 = t + 2 < ucnt ? __builtin_amdgcn_readfirstlane(e2v) : 0u;
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
+        em2 = em1;
+        em1 = e0;
+        e0 = e1;
+        e1 = e2;
     }
-    // group 1's count of the last tile (interval ucnt) is flushed here
-    if (g == 1 && ucnt > 0) {
-        const uint32_t ef = entry(ucnt - 1);
-        const int jf = (int)(ef & 0xFFFF);
-        if (((ef >> 17) & 1u) != 0) flush((ucnt - 1) & 1, jf, min(BS, L - jf * BS));
-    }
+    // group 1's count of the last tile (interval ucnt; its entry is in em2
+    // after the last rotation) is flushed here
+    if (g == 1 && qw == 0 && ucnt > 0 && ((em2 >> 17) & 1u) != 0) flush(1, (ucnt - 1) & 1, (int)(em2 & 0xFFFF));
 }
 
 template <int D, int BS>
