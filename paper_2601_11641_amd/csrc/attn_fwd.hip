@@ -62,21 +62,6 @@ __device__ __forceinline__ float max_across_halves(float x) {
     return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
-// Sum of an int over the 64 lanes of a wave (every lane receives it) with
-// DPP moves only (no LDS traffic): pairs, quads, half rows and rows by lane
-// permutations, then rows 1 and 3 add the row before them (row_bcast:15)
-// and rows 2 and 3 add lane 31 (row_bcast:31), which leaves the total in
-// lane 63.
-__device__ __forceinline__ int wave_sum(int x) {
-    x += __builtin_amdgcn_update_dpp(0, x, 0xb1, 0xf, 0xf, false);    // quad_perm [1,0,3,2]
-    x += __builtin_amdgcn_update_dpp(0, x, 0x4e, 0xf, 0xf, false);    // quad_perm [2,3,0,1]
-    x += __builtin_amdgcn_update_dpp(0, x, 0x141, 0xf, 0xf, false);   // row_half_mirror
-    x += __builtin_amdgcn_update_dpp(0, x, 0x140, 0xf, 0xf, false);   // row_mirror
-    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);   // row_bcast:15 into rows 1, 3
-    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);   // row_bcast:31 into rows 2, 3
-    return __builtin_amdgcn_readlane(x, 63);
-}
-
 // Direct-to-LDS copy of 16 bytes per lane: lane l writes LDS bytes
 // [lds + 16 l, +16) with the 16 bytes at sbase + voff (sbase wave-uniform,
 // voff the lane's byte offset).  Written as inline assembly so that the
@@ -1267,8 +1252,8 @@ hipError_t launch(const uint16_t* q, const uint16_t* k, const uint16_t* v, const
 // waves (32 query rows each), so every K tile copied into LDS serves both
 // blocks (double-buffered, every wave copying its share of the next tile).
 // Per tile each wave computes S^T = K Q^T for its 32 query rows by MFMA and
-// counts its entries that reach the row's threshold (per lane, then summed
-// over the wave).  The groups are skewed by one tile with a single
+// counts its entries that reach the row's threshold (one 64-lane compare
+// mask per score, counted and summed on the scalar unit).  The groups are skewed by one tile with a single
 // work-group barrier per tile: in the interval of tile t group 0 multiplies
 // tile t and then counts it, while group 1 first counts tile t-1 (its scores
 // kept in registers) and then multiplies tile t, so on each SIMD one wave's
@@ -1367,12 +1352,36 @@ __global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
                     sacc[rt][ii] = (8 * (ii >> 2) + (ii & 3) >= lim) ? -INFINITY : sacc[rt][ii];
             }
         }
+        // the wave's count: one compare mask per score (64 lanes), counted
+        // and summed on the scalar unit, four scores per block
         int c = 0;
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-            for (int ii = 0; ii < 16; ++ii) c += sacc[rt][ii] >= thr ? 1 : 0;
-        return c;   // this lane's count; wave_sum() totals it
+            for (int ii = 0; ii < 16; ii += 4) {
+                uint64_t m0, m1, m2, m3;
+                int b0, b1;
+                asm volatile(
+                    "v_cmp_ge_f32_e64 %[m0], %[x0], %[t]\n\t"
+                    "v_cmp_ge_f32_e64 %[m1], %[x1], %[t]\n\t"
+                    "v_cmp_ge_f32_e64 %[m2], %[x2], %[t]\n\t"
+                    "v_cmp_ge_f32_e64 %[m3], %[x3], %[t]\n\t"
+                    "s_nop 3\n\t"
+                    "s_bcnt1_i32_b64 %[b0], %[m0]\n\t"
+                    "s_bcnt1_i32_b64 %[b1], %[m1]\n\t"
+                    "s_add_u32 %[c], %[c], %[b0]\n\t"
+                    "s_bcnt1_i32_b64 %[b0], %[m2]\n\t"
+                    "s_add_u32 %[c], %[c], %[b1]\n\t"
+                    "s_bcnt1_i32_b64 %[b1], %[m3]\n\t"
+                    "s_add_u32 %[c], %[c], %[b0]\n\t"
+                    "s_add_u32 %[c], %[c], %[b1]"
+                    : [c] "+s"(c), [m0] "=&s"(m0), [m1] "=&s"(m1), [m2] "=&s"(m2), [m3] "=&s"(m3),
+                      [b0] "=&s"(b0), [b1] "=&s"(b1)
+                    : [x0] "v"(sacc[rt][ii]), [x1] "v"(sacc[rt][ii + 1]), [x2] "v"(sacc[rt][ii + 2]),
+                      [x3] "v"(sacc[rt][ii + 3]), [t] "v"(thr)
+                    : "scc");
+            }
+        return c;   // the wave's count
     };
     // group gg's count of a finished tile (block 2p+gg, kv block j)
     auto flush = [&](int gg, int parity, int j) __attribute__((always_inline)) {
@@ -1416,7 +1425,7 @@ __global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
                 __builtin_amdgcn_s_setprio(1);
                 multiply(cur);
                 __builtin_amdgcn_s_setprio(0);
-                const int c = wave_sum(count(vc));
+                const int c = count(vc);
                 if (lane == 0) part[t & 1][0][qw] = c;
             }
             if (qw == 0) {
@@ -1434,10 +1443,7 @@ __global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
                 multiply(cur);
                 __builtin_amdgcn_s_setprio(0);
             }
-            if (pm) {
-                c = wave_sum(c);
-                if (lane == 0) part[(t - 1) & 1][1][qw] = c;
-            }
+            if (pm && lane == 0) part[(t - 1) & 1][1][qw] = c;
         }
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) asm volatile("" : "+v"(sacc[rt]));
