@@ -47,6 +47,9 @@ CONFIGS = {
     "small3": _cfg("small", H=3),
     # ragged: short tail block, frames straddling blocks
     "ragged": _cfg("small", name="ragged", B=2, H=2, frames=5, hs=9, ws=25, seed=5),
+    # the other two (d, block) forms of the count kernel: n = 19 (tail 48), n = 10 (tail 108)
+    "d128b64": _cfg("small", name="d128b64", B=1, H=2, frames=6, hs=10, ws=20, block=64, seed=6),
+    "d64b128": _cfg("tiny", name="d64b128", B=1, H=2, frames=7, hs=12, ws=15, block=128, seed=7),
 }
 
 
