@@ -1253,11 +1253,12 @@ hipError_t launch(const uint16_t* q, const uint16_t* k, const uint16_t* v, const
 // blocks (double-buffered, every wave copying its share of the next tile).
 // Per tile each wave computes S^T = K Q^T for its 32 query rows by MFMA and
 // counts its entries that reach the row's threshold (one 64-lane compare
-// mask per score, counted and summed on the scalar unit).  The groups are skewed by one tile with a single
-// work-group barrier per tile: in the interval of tile t group 0 multiplies
-// tile t and then counts it, while group 1 first counts tile t-1 (its scores
-// kept in registers) and then multiplies tile t, so on each SIMD one wave's
-// matrix products run beside the other wave's compares.  A group's count of
+// mask per score, counted and summed on the scalar unit).  The groups are
+// skewed by one tile with a single work-group barrier per tile: in the
+// interval of tile t group 0 multiplies tile t and then counts it, while
+// group 1 first counts tile t-1 (its scores kept in registers) and then
+// multiplies tile t, so on each SIMD one wave's matrix products run beside
+// the other wave's compares.  A group's count of
 // a tile is summed over its waves and written into stat[bh][i][j] (fp64)
 // after the next barrier, by group 0's first wave at the end of its interval
 // (off group 1's path, which bounds the interval); blocks not listed keep
