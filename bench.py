@@ -117,9 +117,33 @@ def parse():
 
 
 def source_digest(path: str = ATTN_SOURCE) -> str:
+    """Digest of a kernel source's code: comments dropped (string and
+    character literals kept as written) and whitespace runs collapsed, so
+    that an edit of the comments alone leaves it unchanged."""
     import hashlib
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    with open(path, encoding="utf-8") as f:
+        text = f.read()
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c in "\"'":
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            out.append(" ")
+            i = n if j < 0 else j + 2
+        else:
+            out.append(c)
+            i += 1
+    code = " ".join("".join(out).split())
+    return hashlib.sha256(code.encode("utf-8")).hexdigest()[:16]
 
 
 TRACE_SUMMARY = os.path.join(ROOT, "profiles", "hunyuan720p_step_kernel_stats.md")
