@@ -234,7 +234,10 @@ bool is_anchor_step(const mod_stats* s, int t) {
 // rhs -> solve of the statistic in G into the next anchor slot
 mod_status fit_stat_into_next_slot(mod_stats* s, int step, hipStream_t st) {
     const int slot = 1 - s->newest;
-    hipError_t e = moddit::launch_rhs(s->G, s->reg, s->r, s->BH, s->n, s->F, st);
+    // the solve's partial-product array u ([kSolveSplit, BH, q], q = n - 1 + F)
+    // is free until the solve and holds the rhs row ranges' sums
+    static_assert(moddit::kRhsChunks * 3 <= moddit::kSolveSplit, "rhs ranges must fit the solve's scratch");
+    hipError_t e = moddit::launch_rhs(s->G, s->reg, s->r, s->u, s->BH, s->n, s->F, st);
     if (e != hipSuccess) return hip_fail(e, "rhs launch");
     e = moddit::launch_solve(s->r, s->reg, s->Sinv, s->bU, s->u, s->X[slot], s->BH, s->n, s->F, st);
     if (e != hipSuccess) return hip_fail(e, "solve launch");

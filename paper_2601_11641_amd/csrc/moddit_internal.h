@@ -12,6 +12,7 @@ namespace moddit {
 
 constexpr int kMaxBlocks = 4096;     // largest n (selection keeps a row in LDS)
 constexpr int kSolveSplit = 16;     // k-chunks of the Schur-complement product (fixed: deterministic sum)
+constexpr int kRhsChunks = 4;       // row ranges of the right-hand side sums (fixed: deterministic sum)
 
 // a1: block means of Q and K, fp64 [BH, n, d], over the first L tokens of
 // each head (L_stride tokens apart).
@@ -26,7 +27,8 @@ hipError_t launch_block_mass(const double* qbar, const double* kbar, double* G, 
 // solve into X [BH, p].  reg: [F][2] inclusive block ranges; Sinv: inverse
 // of the Schur complement [q, q], q = n - 1 + F; bU: scratch [BH, q];
 // u: scratch [kSolveSplit, BH, q] (partial products per k-chunk).
-hipError_t launch_rhs(const double* G, const int* reg, double* r, int BH, int n, int F,
+// part: scratch of kRhsChunks * BH * (3n - 1) doubles (the row ranges' sums).
+hipError_t launch_rhs(const double* G, const int* reg, double* r, double* part, int BH, int n, int F,
                       hipStream_t s);
 hipError_t launch_solve(const double* r, const int* reg, const double* Sinv, double* bU,
                         double* u, double* X, int BH, int n, int F, hipStream_t s);

@@ -230,50 +230,68 @@ __global__ __launch_bounds__(kThreads) void logits_kernel(const double* __restri
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void mass_softmax_kernel(double* __restrict__ G, int L,
                                                                 int bs, int n) {
+    constexpr int NPT = kMaxBlocks / kThreads;   // row entries per thread at most
     __shared__ double red[kThreads];
     double* g = G + (size_t)blockIdx.x * n;
+    // the row is read once into registers (entry j = threadIdx.x + c kThreads)
+    double x[NPT];
     double m = -INFINITY;
-    for (int j = threadIdx.x; j < n; j += kThreads) m = fmax(m, g[j]);
+#pragma unroll
+    for (int c = 0; c < NPT; ++c) {
+        const int j = threadIdx.x + c * kThreads;
+        x[c] = j < n ? g[j] : -INFINITY;
+        m = fmax(m, x[c]);
+    }
     m = block_max(m, red);
     double s = 0.0;
-    for (int j = threadIdx.x; j < n; j += kThreads) {
-        const double w = static_cast<double>(min(bs, L - j * bs)) * exp(g[j] - m);
-        g[j] = w;
-        s += w;
+#pragma unroll
+    for (int c = 0; c < NPT; ++c) {
+        const int j = threadIdx.x + c * kThreads;
+        if (j < n) {
+            x[c] = static_cast<double>(min(bs, L - j * bs)) * exp(x[c] - m);
+            s += x[c];
+        }
     }
     s = block_sum(s, red);
-    for (int j = threadIdx.x; j < n; j += kThreads) g[j] = g[j] / s;
+#pragma unroll
+    for (int c = 0; c < NPT; ++c) {
+        const int j = threadIdx.x + c * kThreads;
+        if (j < n) g[j] = x[c] / s;
+    }
 }
 
 // ---------------------------------------------------------------------------
 // a3 (rhs): r = M^T vec(G): diagonal sums (2n-1), column sums (n) and frame
-// square sums (F).  Diagonals and columns: one thread per output, its
-// entries taken in row order into four interleaved partial sums (rows i mod
-// 4) combined as (s0 + s1) + (s2 + s3); consecutive threads read
-// consecutive addresses.  Frame squares: one work-group per (frame, head),
-// a fixed assignment of entries to threads and a fixed-order tree.  Every
-// sum has a fixed order, so the result is deterministic.
+// square sums (F).  Diagonals and columns: the rows split into kRhsChunks
+// fixed ranges; per (output, range) one thread takes the range's entries in
+// row order into four interleaved partial sums (rows i mod 4) combined as
+// (s0 + s1) + (s2 + s3), consecutive threads reading consecutive addresses;
+// the ranges' sums are then added in range order.  Frame squares: one
+// work-group per (frame, head), a fixed assignment of entries to threads and
+// a fixed-order tree.  Every sum has a fixed order, so the result is
+// deterministic.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void rhs_kernel(const double* __restrict__ G,
-                                                       double* __restrict__ r, int n, int F) {
-    const int bh = blockIdx.y;
+                                                       double* __restrict__ part, int BH, int n) {
+    const int bh = blockIdx.z, ch = blockIdx.y;
     const int o = blockIdx.x * kThreads + threadIdx.x;
-    const int p = 3 * n - 1 + F;
     if (o >= 3 * n - 1) return;
     const double* g = G + (size_t)bh * n * n;
+    // rows [ch n / kRhsChunks, (ch + 1) n / kRhsChunks) of the output's entries
+    const int r0 = (int)((long long)ch * n / kRhsChunks), r1 = (int)((long long)(ch + 1) * n / kRhsChunks) - 1;
     int i0, i1;
     size_t step, at;
     if (o < 2 * n - 1) {                 // diagonal j - i = dl
         const int dl = o - (n - 1);
-        i0 = max(0, -dl);
-        i1 = min(n - 1, n - 1 - dl);
+        i0 = max(r0, max(0, -dl));
+        i1 = min(r1, min(n - 1, n - 1 - dl));
         step = (size_t)n + 1;
         at = (size_t)i0 * n + i0 + dl;
     } else {                             // column j
-        i0 = 0;
-        i1 = n - 1;
+        i0 = r0;
+        i1 = r1;
         step = (size_t)n;
-        at = (size_t)(o - (2 * n - 1));
+        at = (size_t)i0 * n + (o - (2 * n - 1));
     }
     double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
     int i = i0;
@@ -288,7 +306,19 @@ __global__ __launch_bounds__(kThreads) void rhs_kernel(const double* __restrict_
         else if (q == 1) s1 += g[at];
         else s2 += g[at];
     }
-    r[(size_t)bh * p + o] = (s0 + s1) + (s2 + s3);
+    part[((size_t)ch * BH + bh) * (3 * n - 1) + o] = (s0 + s1) + (s2 + s3);
+}
+
+// The ranges' sums of every diagonal and column, added in range order.
+__global__ __launch_bounds__(kThreads) void rhs_sum_kernel(const double* __restrict__ part,
+                                                           double* __restrict__ r, int BH, int n, int F) {
+    const int bh = blockIdx.y;
+    const int o = blockIdx.x * kThreads + threadIdx.x;
+    if (o >= 3 * n - 1) return;
+    double s = part[(size_t)bh * (3 * n - 1) + o];
+#pragma unroll
+    for (int ch = 1; ch < kRhsChunks; ++ch) s += part[((size_t)ch * BH + bh) * (3 * n - 1) + o];
+    r[(size_t)bh * (3 * n - 1 + F) + o] = s;
 }
 
 __global__ __launch_bounds__(kThreads) void rhs_frame_kernel(const double* __restrict__ G,
@@ -1017,10 +1047,14 @@ hipError_t launch_block_mass(const double* qbar, const double* kbar, double* G, 
     return hipGetLastError();
 }
 
-hipError_t launch_rhs(const double* G, const int* reg, double* r, int BH, int n, int F,
+hipError_t launch_rhs(const double* G, const int* reg, double* r, double* part, int BH, int n, int F,
                       hipStream_t s) {
-    hipLaunchKernelGGL(rhs_kernel, dim3(cdiv(3 * n - 1, kThreads), BH), dim3(kThreads), 0, s, G, r, n, F);
+    hipLaunchKernelGGL(rhs_kernel, dim3(cdiv(3 * n - 1, kThreads), kRhsChunks, BH), dim3(kThreads), 0, s, G, part,
+                       BH, n);
     hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(rhs_sum_kernel, dim3(cdiv(3 * n - 1, kThreads), BH), dim3(kThreads), 0, s, part, r, BH, n, F);
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(rhs_frame_kernel, dim3(F, BH), dim3(kThreads), 0, s, G, reg, r, n, F);
     return hipGetLastError();
