@@ -74,6 +74,24 @@ __device__ T block_exclusive_scan(T v, T* wsum, T* total) {
     return base + (incl - v);
 }
 
+// In-place inclusive prefix sum of a[0 .. len) in LDS over one work-group:
+// thread t scans its contiguous segment, the segment totals are scanned in
+// thread order, and each segment adds its offset (a fixed order).  Every
+// thread of the work-group calls it; a is complete on return.
+__device__ void block_inclusive_prefix(double* a, int len, double* wsum) {
+    const int seg = (len + kThreads - 1) / kThreads;
+    const int b0 = min(len, (int)threadIdx.x * seg), b1 = min(len, b0 + seg);
+    double run = 0.0;
+    for (int b = b0; b < b1; ++b) {
+        run += a[b];
+        a[b] = run;
+    }
+    double total;
+    const double off = block_exclusive_scan<double>(run, wsum, &total);
+    for (int b = b0; b < b1; ++b) a[b] += off;
+    __syncthreads();
+}
+
 // ---------------------------------------------------------------------------
 // a1: block pooling.  Grid (n, BH, 2): z = 0 pools Q, z = 1 pools K.  The
 // block is one contiguous run of rows*D bf16.  Lane l of wave w reads the
@@ -350,29 +368,29 @@ __global__ __launch_bounds__(kThreads) void solve_pre_kernel(const double* __res
                                                              const int* __restrict__ reg,
                                                              double* __restrict__ bU, int n,
                                                              int F) {
-    extern __shared__ double y[];   // 2n - 1
+    extern __shared__ double y[];   // 2n - 1: Dc^{-1} r_C, then its inclusive prefix
+    __shared__ double wsum[kThreads / 64];
     const int bh = blockIdx.y;      // x: a chunk of kThreads outputs
     const int p = 3 * n - 1 + F, q = n - 1 + F;
     const double* rr = r + (size_t)bh * p;
     for (int a = threadIdx.x; a < 2 * n - 1; a += kThreads)
         y[a] = rr[a] / static_cast<double>(n - abs(a - (n - 1)));
     __syncthreads();
-    {
-        const int j = blockIdx.x * kThreads + threadIdx.x;
-        if (j >= q) return;
-        double s = 0.0, b;
-        if (j < n - 1) {
-            for (int a = j; a <= j + n - 1; ++a) s += y[a];
-            b = rr[2 * n - 1 + j];
-        } else {
-            const int f = j - (n - 1);
-            const int sz = reg[2 * f + 1] - reg[2 * f] + 1;
-            for (int dl = -(sz - 1); dl <= sz - 1; ++dl)
-                s += static_cast<double>(sz - abs(dl)) * y[dl + n - 1];
-            b = rr[3 * n - 1 + f];
-        }
-        bU[(size_t)bh * q + j] = b - s;
+    const int j = blockIdx.x * kThreads + threadIdx.x;
+    // frame rows of W^T: weighted sums of the diagonals a frame square spans
+    double s = 0.0;
+    if (j >= n - 1 && j < q) {
+        const int f = j - (n - 1);
+        const int sz = reg[2 * f + 1] - reg[2 * f] + 1;
+        for (int dl = -(sz - 1); dl <= sz - 1; ++dl)
+            s += static_cast<double>(sz - abs(dl)) * y[dl + n - 1];
     }
+    __syncthreads();
+    // column rows of W^T: the n diagonals column j crosses, y[j .. j + n - 1],
+    // as a difference of the prefix sums
+    block_inclusive_prefix(y, 2 * n - 1, wsum);
+    if (j < n - 1) s = y[j + n - 1] - (j > 0 ? y[j - 1] : 0.0);
+    if (j < q) bU[(size_t)bh * q + j] = (j < n - 1 ? rr[2 * n - 1 + j] : rr[3 * n - 1 + (j - (n - 1))]) - s;
 }
 
 // u[h] = S^{-1} bU[h] for all heads, split over kSolveSplit fixed chunks of
@@ -386,6 +404,8 @@ __global__ __launch_bounds__(kThreads) void solve_gemv_kernel(const double* __re
                                                               double* __restrict__ part, int q,
                                                               int BH) {
     constexpr int HW = 8;
+    // a wave's right-hand sides, 64 k at a time: bs[w][k - kb][hh]
+    __shared__ double bs[kThreads / 64][64][HW];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int j = blockIdx.x * 64 + lane;
     const int c = blockIdx.y;
@@ -395,13 +415,23 @@ __global__ __launch_bounds__(kThreads) void solve_gemv_kernel(const double* __re
         double acc[HW];
 #pragma unroll
         for (int hh = 0; hh < HW; ++hh) acc[hh] = 0.0;
-        if (j < q) {
-            for (int k = k0; k < k1; ++k) {
-                const double a = Sinv[(size_t)k * q + j];
+        for (int kb = k0; kb < k1; kb += 64) {
+            const int kn = min(64, k1 - kb);
+            // (the wave's LDS operations run in order: the previous pass's
+            // reads are done before these writes)
 #pragma unroll
-                for (int hh = 0; hh < HW; ++hh)
-                    if (h0 + hh < BH) acc[hh] = fma(a, bU[(size_t)(h0 + hh) * q + k], acc[hh]);
+            for (int hh = 0; hh < HW; ++hh)
+                bs[w][lane][hh] = (lane < kn && h0 + hh < BH) ? bU[(size_t)(h0 + hh) * q + kb + lane] : 0.0;
+            if (j < q) {
+#pragma unroll 4
+                for (int kk = 0; kk < kn; ++kk) {
+                    const double a = Sinv[(size_t)(kb + kk) * q + j];
+#pragma unroll
+                    for (int hh = 0; hh < HW; ++hh) acc[hh] = fma(a, bs[w][kk][hh], acc[hh]);
+                }
             }
+        }
+        if (j < q) {
 #pragma unroll
             for (int hh = 0; hh < HW; ++hh)
                 if (h0 + hh < BH) part[((size_t)c * BH + h0 + hh) * q + j] = acc[hh];
@@ -414,34 +444,46 @@ __global__ __launch_bounds__(kThreads) void solve_post_kernel(const double* __re
                                                               const int* __restrict__ reg,
                                                               double* __restrict__ X, int n,
                                                               int F, int BH) {
-    extern __shared__ double us[];   // q
-    const int bh = blockIdx.y;       // x: a chunk of kThreads outputs of X
+    extern __shared__ double us[];   // q: u, then the prefix of its first n - 1 entries; then F frame sizes
+    __shared__ double wsum[kThreads / 64];
+    __shared__ int szmax;
+    const int bh = blockIdx.x;       // one work-group per head
     const int p = 3 * n - 1 + F, q = n - 1 + F;
-    // u = sum of the k-chunk partial products, in chunk order
+    int* sz = reinterpret_cast<int*>(us + q);
+    if (threadIdx.x == 0) szmax = 0;
+    __syncthreads();
+    for (int f = threadIdx.x; f < F; f += kThreads) {
+        sz[f] = reg[2 * f + 1] - reg[2 * f] + 1;
+        atomicMax(&szmax, sz[f]);
+    }
+    const double* rr = r + (size_t)bh * p;
+    double* x = X + (size_t)bh * p;
+    // u = sum of the k-chunk partial products, in chunk order; the d and e
+    // parts of X are u itself
     for (int a = threadIdx.x; a < q; a += kThreads) {
         double v = 0.0;
         for (int c = 0; c < kSolveSplit; ++c) v += u[((size_t)c * BH + bh) * q + a];
         us[a] = v;
+        if (a < n - 1) x[2 * n - 1 + a] = v;
+        else x[3 * n - 1 + (a - (n - 1))] = v;
     }
+    if (threadIdx.x == 0) x[3 * n - 2] = 0.0;   // d_{n-1}: the gauge column dropped
     __syncthreads();
-    const double* rr = r + (size_t)bh * p;
-    double* x = X + (size_t)bh * p;
-    const int a = blockIdx.x * kThreads + threadIdx.x;
-    if (a < 2 * n - 1) {
+    block_inclusive_prefix(us, n - 1, wsum);
+    // c = Dc^{-1} (r_C - W u): the columns crossing diagonal dl are a window
+    // of d (a difference of the prefix sums), the frames' weights max(0,
+    // |R_f| - |dl|) multiply e
+    for (int a = threadIdx.x; a < 2 * n - 1; a += kThreads) {
         const int dl = a - (n - 1);
-        double s = 0.0;
         const int j0 = max(0, dl), j1 = min(n - 2, dl + n - 1);
-        for (int j = j0; j <= j1; ++j) s += us[j];
-        for (int f = 0; f < F; ++f) {
-            const int w = (reg[2 * f + 1] - reg[2 * f] + 1) - abs(dl);
-            if (w > 0) s += static_cast<double>(w) * us[n - 1 + f];
+        double s = j1 >= j0 ? us[j1] - (j0 > 0 ? us[j0 - 1] : 0.0) : 0.0;
+        if (abs(dl) < szmax) {   // only diagonals shorter than a frame square's side meet one
+            for (int f = 0; f < F; ++f) {
+                const int w = sz[f] - abs(dl);
+                if (w > 0) s += static_cast<double>(w) * us[n - 1 + f];
+            }
         }
         x[a] = (rr[a] - s) / static_cast<double>(n - abs(dl));
-    } else if (a < 3 * n - 1) {
-        const int j = a - (2 * n - 1);
-        x[a] = (j < n - 1) ? us[j] : 0.0;
-    } else if (a < p) {
-        x[a] = us[n - 1 + (a - (3 * n - 1))];
     }
 }
 
@@ -1071,8 +1113,8 @@ hipError_t launch_solve(const double* r, const int* reg, const double* Sinv, dou
                        u, q, BH);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(solve_post_kernel, dim3(cdiv(3 * n - 1 + F, kThreads), BH), dim3(kThreads),
-                       (size_t)q * sizeof(double), s, r, u, reg, X, n, F, BH);
+    hipLaunchKernelGGL(solve_post_kernel, dim3(BH), dim3(kThreads), (size_t)q * sizeof(double) + (size_t)F * sizeof(int),
+                       s, r, u, reg, X, n, F, BH);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(solve_gauge_kernel, dim3(BH), dim3(kThreads), 0, s, X, n, F);
