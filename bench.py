@@ -651,7 +651,8 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
-              "the hot path is measured at one GPU's share, see DESIGN.md for sharding.",
+              "the hot path is measured at one GPU's share (bench.py --share); a layer shards by head "
+              "across GPUs with no exchange between them.",
               file=sys.stderr)
         sys.exit(2)
 

@@ -55,7 +55,7 @@ _ANCHOR_LOGIT = 4.0
 
 # Feature RMS.  Chosen once on the 8-frame 32x32 small layer so that, under
 # dense attention, the top 25% of KV blocks of a query block hold at least
-# 80% of its attention mass on average (input recipe).
+# 80% of its attention mass on average.
 KAPPA = 3.0
 
 
