@@ -107,6 +107,10 @@ def parse():
                          "attention time, rate, per-head imbalance and the share's time over the "
                          "kept-work-proportional part of the whole layer's time; one JSON line "
                          "per layer")
+    ap.add_argument("--count", action="store_true",
+                    help="the Eq. 2 count pass of a dense step on the Hunyuan 720p layer alone "
+                         "(mod_update_stats over full lists with the dense attention's LSE): "
+                         "time per update and the rate on its QK^T flops; one JSON line")
     ap.add_argument("--trace-summary", nargs=2, metavar=("STATS_CSV", "BENCH_LOG"),
                     help="format a rocprofv3 --kernel-trace --stats CSV of a bench run (and the JSON "
                          "line that run printed) into profiles/hunyuan720p_step_kernel_stats.md and exit")
@@ -543,6 +547,53 @@ def run_share(args):
         }), flush=True)
 
 
+def run_count(args):
+    """Eq. 2 statistic of a dense step on the Hunyuan 720p layer: one dense
+    attention for the row LSE, then --warmup untimed and --steps timed
+    mod_update_stats calls over the full lists (the count pass recomputes
+    QK^T for every block, then the fit); HIP events on the launch stream."""
+    import numpy as np
+    import torch
+
+    import paper_2601_11641_amd as M
+    import workloads as W
+
+    cfg = W.CONFIGS["hunyuan"]
+    dev = torch.device("cuda:0")
+    host = W.generate(cfg)
+    q, k, v = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev) for x in host)
+    del host
+    shape = M.make_shape(cfg.B, cfg.H, cfg.L, cfg.d, cfg.block, cfg.frame_tokens)
+    stream = torch.cuda.current_stream()
+    n = cfg.n
+    idx = torch.arange(n, dtype=torch.int32, device=dev).repeat(cfg.B * cfg.H * n).reshape(cfg.B, cfg.H, n, n)
+    cnt = torch.full((cfg.B, cfg.H, n), n, dtype=torch.int32, device=dev)
+    out = torch.empty_like(q)
+    lse = torch.empty((cfg.B, cfg.H, cfg.L), dtype=torch.float32, device=dev)
+    M.mod_block_sparse_attn_fwd(shape, q, k, v, idx, cnt, 0.0, out, lse, None, 0, stream)
+    st = M.Stats(shape, M.make_params(warmup_m=1, statistic="attention"))
+    times = []
+    for t in range(1, args.warmup + args.steps + 1):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        M.mod_update_stats(st.handle, q, k, lse, idx, cnt, t, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if t > args.warmup:
+            times.append(e0.elapsed_time(e1))
+    st.close()
+    ms = float(np.median(times))
+    tflop = 2.0 * cfg.d * float(cfg.L) * float(cfg.L) * cfg.B * cfg.H / 1e12
+    print(json.dumps({
+        "workload": f"hunyuan-720p dense Eq. 2 count pass (B={cfg.B} H={cfg.H} L={cfg.L} d={cfg.d} "
+                    f"block={cfg.block}), full lists",
+        "steps": args.steps, "warmup": args.warmup,
+        "update_ms_median": round(ms, 3), "update_ms_min": round(min(times), 3),
+        "qk_tflop": round(tflop, 3), "qk_tflops": round(tflop / (ms / 1e3), 1),
+        "frac_of_bf16_peak": round(tflop / (ms / 1e3) / PEAK_BF16_TFLOPS, 4),
+    }), flush=True)
+
+
 def run_schedule(args):
     """50 denoising steps on the Hunyuan 720p shape: steps 1-5 dense (full
     lists) with statistics collected at steps 4 and 5, steps 6-50 predicted
@@ -670,6 +721,9 @@ def main():
         return
     if args.schedule:
         run_schedule(args)
+        return
+    if args.count:
+        run_count(args)
         return
     if args.share:
         run_share(args)
