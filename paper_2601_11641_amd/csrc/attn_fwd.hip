@@ -1411,41 +1411,19 @@ __global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
     // list entries of tiles t-2 .. t+1 are carried in scalar registers; the
     // entry of tile t+2 is read from LDS at the start of the interval and
     // taken at its end.
+    // Each group runs its own copy of the interval loop (the same barriers in
+    // the same order): group 1's scores live from one interval into the
+    // next and group 0's do not, which one shared loop body would reconcile
+    // by copying the scores at every iteration.
     uint32_t em2 = 0u, em1 = 0u;
     uint32_t e0 = ucnt > 0 ? entry(0) : 0u;
     uint32_t e1 = ucnt > 1 ? entry(1) : 0u;
-    for (int t = 0; t <= ucnt; ++t) {
+    // the part of an interval both groups run first and last
+    auto begin = [&](int t) __attribute__((always_inline)) {
         if (t + 1 < ucnt) copy.issue_all(kg, (int)(e1 & 0xFFFF), L, kbuf[(t + 1) & 1], w, lane);
-        const uint32_t e2v = ulist[min(t + 2, max(ucnt - 1, 0))];
-        const char* cur = kbuf[t & 1];
-        const int jc = (int)(e0 & 0xFFFF);
-        const bool mc = t < ucnt && ((e0 >> (16 + g)) & 1u) != 0;
-        const int vc = min(BS, L - jc * BS);
-        if (g == 0) {
-            if (mc) {
-                __builtin_amdgcn_s_setprio(1);
-                multiply(cur);
-                __builtin_amdgcn_s_setprio(0);
-                const int c = count(vc);
-                if (lane == 0) part[t & 1][0][qw] = c;
-            }
-            if (qw == 0) {
-                if (t >= 1 && ((em1 >> 16) & 1u) != 0) flush(0, (t - 1) & 1, (int)(em1 & 0xFFFF));
-                if (t >= 2 && ((em2 >> 17) & 1u) != 0) flush(1, t & 1, (int)(em2 & 0xFFFF));
-            }
-        } else {
-            // counts of tile t-1 per lane first (they free sacc), the wave's
-            // total after this tile's products are issued
-            int c = 0;
-            const bool pm = t > 0 && ((em1 >> 17) & 1u) != 0;
-            if (pm) c = count(min(BS, L - (int)(em1 & 0xFFFF) * BS));
-            if (mc) {
-                __builtin_amdgcn_s_setprio(1);
-                multiply(cur);
-                __builtin_amdgcn_s_setprio(0);
-            }
-            if (pm && lane == 0) part[(t - 1) & 1][1][qw] = c;
-        }
+        return ulist[min(t + 2, max(ucnt - 1, 0))];
+    };
+    auto end = [&](int t, uint32_t e2v) __attribute__((always_inline)) {
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) asm volatile("" : "+v"(sacc[rt]));
         const uint32_t e2 = t + 2 < ucnt ? __builtin_amdgcn_readfirstlane(e2v) : 0u;
@@ -1455,6 +1433,40 @@ __global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
         em1 = e0;
         e0 = e1;
         e1 = e2;
+    };
+    if (g == 0) {
+        for (int t = 0; t <= ucnt; ++t) {
+            const uint32_t e2v = begin(t);
+            const int jc = (int)(e0 & 0xFFFF);
+            if (t < ucnt && (e0 >> 16 & 1u) != 0) {
+                __builtin_amdgcn_s_setprio(1);
+                multiply(kbuf[t & 1]);
+                __builtin_amdgcn_s_setprio(0);
+                const int c = count(min(BS, L - jc * BS));
+                if (lane == 0) part[t & 1][0][qw] = c;
+            }
+            if (qw == 0) {
+                if (t >= 1 && ((em1 >> 16) & 1u) != 0) flush(0, (t - 1) & 1, (int)(em1 & 0xFFFF));
+                if (t >= 2 && ((em2 >> 17) & 1u) != 0) flush(1, t & 1, (int)(em2 & 0xFFFF));
+            }
+            end(t, e2v);
+        }
+    } else {
+        for (int t = 0; t <= ucnt; ++t) {
+            const uint32_t e2v = begin(t);
+            // counts of tile t-1 first (they free the scores), then this
+            // tile's products
+            int c = 0;
+            const bool pm = t > 0 && ((em1 >> 17) & 1u) != 0;
+            if (pm) c = count(min(BS, L - (int)(em1 & 0xFFFF) * BS));
+            if (t < ucnt && (e0 >> 17 & 1u) != 0) {
+                __builtin_amdgcn_s_setprio(1);
+                multiply(kbuf[t & 1]);
+                __builtin_amdgcn_s_setprio(0);
+            }
+            if (pm && lane == 0) part[(t - 1) & 1][1][qw] = c;
+            end(t, e2v);
+        }
     }
     // group 1's count of the last tile (interval ucnt; its entry is in em2
     // after the last rotation) is flushed here
