@@ -207,6 +207,16 @@ __device__ __forceinline__ void wait_vmcnt() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// f(integral_constant<int, i>) for i = 0 .. N-1, unrolled at compile time.
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
 // ---------------------------------------------------------------------------
 // Work plan.  The per-pair work (about the two rows' list lengths) varies
 // along the sequence and across heads, so a fixed pair -> XCD map leaves
@@ -736,10 +746,13 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     constexpr int HALF = KVW * ROWB;   // bytes per half tile
     using Copy = TileCopy<D, BS, QW>;
     constexpr int IPW = Copy::IPW;
-    __shared__ __align__(1024) char kb0[TILE];
-    __shared__ __align__(1024) char kb1[TILE];
-    __shared__ __align__(1024) char vb0[TILE];
-    __shared__ __align__(1024) char vb1[TILE];
+    // K and V tile buffers, at fixed distances: the matrix-phase reads name
+    // a buffer by a constant offset
+    __shared__ __align__(1024) char tiles[4 * TILE];
+    char* const kb0 = tiles;
+    char* const kb1 = tiles + TILE;
+    char* const vb0 = tiles + 2 * TILE;
+    char* const vb1 = tiles + 3 * TILE;
     __shared__ uint32_t ulist[kMaxBlocks];     // union of the two lists: j | membership << 16
     __shared__ uint8_t umask[kMaxBlocks];
     __shared__ int wsum[2 * NT / 64];
@@ -835,6 +848,25 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     const int half8 = (s16 & 1) << 3;
     const int va = tr_row * ROWB + ((c0 ^ swz<D>(tr_row)) << 4) + half8;
     const int vb = (tr_row + 8) * ROWB + ((c0 ^ swz<D>(tr_row + 8)) << 4) + half8;
+    // LDS addresses of those reads in the current buffers of the shared part
+    // (d-chunk kk of K; d-tile dt of V^T, rows 4h.. and 4h+8..), starting in
+    // kb0 and vb0.  A read adds its half and row offsets as a constant, which
+    // the instruction's offset field holds, so the reads need no address
+    // arithmetic; the tile loop moves these values between the two buffers
+    // of a kind (one addition each per tile instead of one per read and
+    // phase).
+    uint32_t kad[KK], vad[2 * DT];
+    {
+        const uint32_t kb0a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)kb0;
+        const uint32_t vb0a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)vb0;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) kad[kk] = kb0a + (uint32_t)(ka ^ (32 * kk));
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            vad[2 * dt] = vb0a + (uint32_t)(va ^ (64 * dt));
+            vad[2 * dt + 1] = vb0a + (uint32_t)(vb ^ (64 * dt));
+        }
+    }
 
     auto barrier = [&]() __attribute__((always_inline)) {
         __builtin_amdgcn_sched_barrier(0);
@@ -845,56 +877,76 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
 
     using yes = std::true_type;
 
-    // M phase of a unit: S^T = K_half Q^T (Kt: the unit's half tile) and the
-    // product of the previous unit, O^T += V^T P^T (Vp: its half tile).  The
-    // two are independent and interleaved; operand loads run PF steps ahead
-    // of their products.
-    auto mphase = [&](const char* Kt, const char* Vp, auto on_tag) __attribute__((always_inline)) {
-        constexpr bool on = decltype(on_tag)::value;
-        if constexpr (on) {
-            // the matrix phase issues first when both waves of a SIMD are ready
-            __builtin_amdgcn_s_setprio(1);
-            constexpr int NS = RT * KK;
-            constexpr int PF = 2;
-            bf16x8 ak[NS], av[NS];
-            auto load = [&](int s) __attribute__((always_inline)) {
-                const int rt = s / KK, kk = s % KK;
-                ak[s] = __builtin_bit_cast(
-                    bf16x8, *reinterpret_cast<const uint4*>(Kt + ((ka ^ (32 * kk)) + 32 * rt * ROWB)));
-                const int cc = s / DT, dt = s % DT;
-                const s16x4 ta = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (lds_s16x4_t*)(Vp + ((va ^ (64 * dt)) + 16 * cc * ROWB)));
-                const s16x4 tb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (lds_s16x4_t*)(Vp + ((vb ^ (64 * dt)) + 16 * cc * ROWB)));
-                const s16x8 v8 = {ta[0], ta[1], ta[2], ta[3], tb[0], tb[1], tb[2], tb[3]};
-                av[s] = __builtin_bit_cast(bf16x8, v8);
-            };
+    // M phase of a unit: S^T = K_half Q^T and the product of the previous
+    // unit, O^T += V^T P^T.  kp(rt, kk) and vp(cc, dt, ab) give the LDS
+    // addresses of the K operand (32-row slice rt, d-chunk kk) and of the
+    // two halves of the V^T operand (16 kv rows cc, d-tile dt).  The two
+    // products are independent and interleaved; operand reads run PF steps
+    // ahead of their products.
+    auto mphase_at = [&](auto&& kp, auto&& vp) __attribute__((always_inline)) {
+        // the matrix phase issues first when both waves of a SIMD are ready
+        __builtin_amdgcn_s_setprio(1);
+        constexpr int NS = RT * KK;
+        constexpr int PF = 2;
+        bf16x8 ak[NS];
+        s16x4 va4[NS], vb4[NS];
+        auto load = [&](auto si) __attribute__((always_inline)) {
+            constexpr int s = decltype(si)::value;
+            constexpr int rt = s / KK, kk = s % KK, cc = s / DT, dt = s % DT;
+            ak[s] = __builtin_bit_cast(bf16x8, *kp(rt, kk));
+            va4[s] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(vp(cc, dt, 0));
+            vb4[s] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(vp(cc, dt, 1));
+        };
+        static_for<PF>(load);
+        static_for<NS>([&](auto si) __attribute__((always_inline)) {
+            constexpr int s = decltype(si)::value;
+            if constexpr (s + PF < NS) load(std::integral_constant<int, s + PF>{});
+            constexpr int rt = s / KK, kk = s % KK, cc = s / DT, dt = s % DT;
+            sacc[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[s], qreg[kk], kk == 0 ? f32x16{} : sacc[rt], 0, 0,
+                                                               0);
+            __builtin_amdgcn_sched_barrier(0);
+            const s16x8 v8 = {va4[s][0], va4[s][1], va4[s][2], va4[s][3],
+                              vb4[s][0], vb4[s][1], vb4[s][2], vb4[s][3]};
+            oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, v8), pb[cc], oacc[dt], 0, 0,
+                                                               0);
+            // keep the operand reads PF steps ahead of their products
+            __builtin_amdgcn_sched_barrier(0);
+        });
+        // the products are issued before the phase ends
 #pragma unroll
-            for (int s = 0; s < PF; ++s) load(s);
+        for (int rt = 0; rt < RT; ++rt) asm volatile("" : "+v"(sacc[rt]));
 #pragma unroll
-            for (int s = 0; s < NS; ++s) {
-                if (s + PF < NS) load(s + PF);
-                const int rt = s / KK, kk = s % KK;
-                sacc[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[s], qreg[kk], kk == 0 ? f32x16{} : sacc[rt],
-                                                                   0, 0, 0);
-                const int cc = s / DT, dt = s % DT;
-                oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[s], pb[cc], oacc[dt], 0, 0, 0);
-                // keep the operand loads PF steps ahead of their products
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            // the products are issued before the phase ends
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt) asm volatile("" : "+v"(sacc[rt]));
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) asm volatile("" : "+v"(oacc[dt]));
-            __builtin_amdgcn_s_setprio(0);
-        }
+        for (int dt = 0; dt < DT; ++dt) asm volatile("" : "+v"(oacc[dt]));
+        __builtin_amdgcn_s_setprio(0);
+    };
+    typedef __attribute__((address_space(3))) const uint4 lds_u4_t;
+    // In the shared part: the K half tile KO bytes and the V half tile VO
+    // bytes past the current buffers (kad, vad).
+    auto mphase = [&](auto ko_tag, auto vo_tag) __attribute__((always_inline)) {
+        constexpr int KO = decltype(ko_tag)::value, VO = decltype(vo_tag)::value;
+        mphase_at(
+            [&](int rt, int kk) __attribute__((always_inline)) {
+                return (lds_u4_t*)(uintptr_t)(kad[kk] + (uint32_t)(KO + 32 * rt * ROWB));
+            },
+            [&](int cc, int dt, int ab) __attribute__((always_inline)) {
+                return (lds_s16x4_t*)(uintptr_t)(vad[2 * dt + ab] + (uint32_t)(VO + 16 * cc * ROWB));
+            });
+    };
+    // In the exclusive part: the half tiles Kt and Vp of the group's buffers.
+    auto mphase_rt = [&](const char* Kt, const char* Vp) __attribute__((always_inline)) {
+        mphase_at(
+            [&](int rt, int kk) __attribute__((always_inline)) {
+                return reinterpret_cast<const uint4*>(Kt + ((ka ^ (32 * kk)) + 32 * rt * ROWB));
+            },
+            [&](int cc, int dt, int ab) __attribute__((always_inline)) {
+                return (lds_s16x4_t*)(Vp + (((ab ? vb : va) ^ (64 * dt)) + 16 * cc * ROWB));
+            });
     };
     // The M phase of a unit runs both products unless neither is needed
     // (its tile and the previous one are missing from this group's list); an
     // unneeded one multiplies a zero P, or produces scores nobody reads.
     auto mphase_if = [&](const char* Kt, const char* Vp, bool s_on, bool pv_on) __attribute__((always_inline)) {
-        if (s_on || pv_on) mphase(Kt, Vp, yes{});
+        if (s_on || pv_on) mphase_rt(Kt, Vp);
     };
     auto zero_p = [&]() __attribute__((always_inline)) {
 #pragma unroll
@@ -1026,12 +1078,31 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     bool prev_active = false;   // the previous tile is in this group's list
     // Every block of this part is in both lists: both groups run every phase
     // (the first product multiplies P = 0).
-    auto tile = [&](int t, char* kc, char* kn, char* vc, char* vp) __attribute__((always_inline)) {
+    // The K and V buffers alternate from tile to tile.  The matrix-phase
+    // reads take the current buffers from kad (K(t)) and vad: V(t-1) in the
+    // first unit, V(t) after a move in the second; kad moves at the end of
+    // the tile.  A move adds +TILE or -TILE (the distance between the two
+    // buffers of a kind), one instruction per address per tile.
+    using IC0 = std::integral_constant<int, 0>;
+    using ICH = std::integral_constant<int, HALF>;
+    auto move = [&](uint32_t* a, int cnt, int by) __attribute__((always_inline)) {
+#pragma unroll
+        for (int c = 0; c < cnt; ++c) {
+            a[c] += (uint32_t)by;
+            asm volatile("" : "+v"(a[c]));
+        }
+    };
+    move(vad, 2 * DT, TILE);   // the first tile's "previous" V half is vb1's (zeroed)
+    int mv = TILE;             // kb0 -> kb1 (and vb1 -> vb0) in tile t0, the reverse in t0+1, ...
+    char* kn = kb1;            // copy targets: the next tile's K and V buffers
+    char* vp = vb1;
+    auto tile = [&](int t) __attribute__((always_inline)) {
         const bool more = t + 1 < t1;
         const int jc = (int)(e_cur & 0xFFFF), jn = (int)(e_nxt & 0xFFFF);
         const int kvalid = min(BS, L - jc * BS);
         // first half: S from K(t) rows [0, KVW); product of V(t-1) rows [KVW, BS)
-        mphase(kc, vp + HALF, yes{});
+        mphase(IC0{}, ICH{});
+        move(vad, 2 * DT, -mv);
         if (g == 1) wait_copies();
         barrier();
         // copy of the next tile (a short one is issued at once by start())
@@ -1041,33 +1112,24 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
                [&](int c) __attribute__((always_inline)) { copy.issue_one(cg, c, ct, qw); });
         barrier();
         // second half: S from K(t) rows [KVW, BS); product of V(t) rows [0, KVW)
-        mphase(kc + HALF, vc, yes{});
+        mphase(ICH{}, IC0{});
         barrier();
         uint32_t e_after = t + 2 < t1 ? ulist[t + 2] : 0u;
         e_after = __builtin_amdgcn_readfirstlane(e_after);
         xphase(kvalid, std::integral_constant<int, 1>{}, false, no_copy);
         if (g == 0) wait_copies();
         barrier();
+        move(kad, KK, mv);
+        mv = -mv;
+        kn = kn == kb1 ? kb0 : kb1;
+        vp = vp == vb1 ? vb0 : vb1;
         e_cur = e_nxt;
         e_nxt = e_after;
     };
-    // The copies are inline assembly, invisible to the compiler's alias
-    // analysis, so the buffers simply rotate at run time.
-    char* kc = kb0;
-    char* kn = kb1;
-    char* vc = vb0;
-    char* vp = vb1;
-    for (int t = t0; t < t1; ++t) {
-        tile(t, kc, kn, vc, vp);
-        char* tmp = kc;
-        kc = kn;
-        kn = tmp;
-        tmp = vc;
-        vc = vp;
-        vp = tmp;
-    }
-    // the pending product of the last tile's second half (its V now in vp)
-    if (t1 > t0) mphase(kc, vp + HALF, yes{});
+    for (int t = t0; t < t1; ++t) tile(t);
+    // the pending product of the last tile's second half (V rows [KVW, BS)
+    // of the last tile's V buffer; the scores of that phase go unread)
+    if (t1 > t0) mphase(IC0{}, ICH{});
     if (g == 0) barrier();   // both groups pass the same number of barriers
 
     // ---- blocks in one list only: both groups at once ----
@@ -1167,7 +1229,7 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
             ec = en;
             en = ea;
         }
-        if (prev_active) mphase(kbuf, vbuf + HALF, yes{});
+        if (prev_active) mphase_rt(kbuf, vbuf + HALF);
         if (g == 0) barrier();
     }
 
