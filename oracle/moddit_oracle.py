@@ -49,12 +49,19 @@ import numpy as np
 
 
 def num_blocks(L: int, bs: int) -> int:
-    """n = ceil(L / B): blocks per dimension (Section 4.1, with a ragged tail)."""
+    """n = ceil(L / B): blocks per dimension (Section 4.1, with a ragged tail).
+
+    Pinned by test_frame_regions_aligned_and_overlapping (the last frame
+    region of the 118,800-token layer ends at block n - 1) and
+    test_kept_block_flops_full_mask_is_dense_count."""
     return -(-L // bs)
 
 
 def block_sizes(L: int, bs: int) -> np.ndarray:
-    """|j| = number of valid tokens of block j (the last one may be short)."""
+    """|j| = number of valid tokens of block j (the last one may be short).
+
+    Pinned by test_block_mass_tail_is_mean_field_token_mass (a short tail
+    weighted by its token count) and test_pool_bruteforce_ragged."""
     n = num_blocks(L, bs)
     return np.array([min(bs, L - j * bs) for j in range(n)], dtype=np.int64)
 
@@ -74,7 +81,10 @@ def frame_regions(L: int, bs: int, frame_tokens: int):
 
 
 def num_coeffs(n: int, F: int) -> int:
-    """|X| = 3n - 1 + |A| (Eq. 4)."""
+    """|X| = 3n - 1 + |A| (Eq. 4).
+
+    Pinned by test_flop_table_matches_paper (the solve counts of the Appendix
+    C table follow from p)."""
     return 3 * n - 1 + F
 
 
@@ -123,20 +133,31 @@ def block_mass(qbar: np.ndarray, kbar: np.ndarray, sizes: np.ndarray, scale: flo
 
 
 def basis_C(n: int, delta: int) -> np.ndarray:
-    """Parallel-to-main-diagonal basis: 1 where j - i = delta (Appendix B.3)."""
+    """Parallel-to-main-diagonal basis: 1 where j - i = delta (Appendix B.3).
+
+    Pinned by
+    test_pattern_index_convention_picks_the_planted_diagonal_and_column and
+    test_null_space_is_z."""
     i, j = np.indices((n, n))
     return (j - i == delta).astype(np.float64)
 
 
 def basis_D(n: int, col: int) -> np.ndarray:
-    """Vertical basis: 1 on column ``col`` (Appendix B.3)."""
+    """Vertical basis: 1 on column ``col`` (Appendix B.3).
+
+    Pinned by
+    test_pattern_index_convention_picks_the_planted_diagonal_and_column and
+    test_null_space_is_z."""
     m = np.zeros((n, n))
     m[:, col] = 1.0
     return m
 
 
 def basis_E(n: int, lo: int, hi: int) -> np.ndarray:
-    """Block-diagonal basis: 1 on the square [lo, hi] x [lo, hi] (Appendix B.3)."""
+    """Block-diagonal basis: 1 on the square [lo, hi] x [lo, hi] (Appendix B.3).
+
+    Pinned by test_normal_matrix_blocks_printed_in_paper (the closed-form
+    blocks of Appendix B.4) and test_null_space_is_z."""
     m = np.zeros((n, n))
     m[lo:hi + 1, lo:hi + 1] = 1.0
     return m
@@ -147,6 +168,9 @@ def design_matrix(n: int, regions) -> np.ndarray:
 
     vec() is row-major.  Column order: diagonal offsets -(n-1)..(n-1),
     then columns 0..n-1, then frame regions.  Only for small n.
+
+    Pinned by test_null_space_is_z (SVD nullity one, spanned by the z of
+    Appendix B.5) and test_normal_matrix_blocks_printed_in_paper.
     """
     cols = [basis_C(n, dl).ravel() for dl in range(-(n - 1), n)]
     cols += [basis_D(n, j).ravel() for j in range(n)]
@@ -227,25 +251,37 @@ def solve_min_norm(N: np.ndarray, r: np.ndarray, n: int, F: int) -> np.ndarray:
 
 def fit(G: np.ndarray, regions) -> np.ndarray:
     """X = [c (2n-1), d (n), e (F)] minimising ||vec(G) - M X|| (Eq. 4),
-    minimum-norm.  G: [n, n]."""
+    minimum-norm.  G: [n, n].
+
+    Pinned by test_fit_equals_lstsq_minimum_norm,
+    test_planted_coefficients_recovered and
+    test_ridge_solution_close_to_minimum_norm."""
     n = G.shape[0]
     return solve_min_norm(normal_matrix(n, regions), rhs(G, regions), n, len(regions))
 
 
 def fit_lstsq(G: np.ndarray, regions) -> np.ndarray:
     """The same fit through the explicit design matrix and LAPACK's SVD
-    least squares (textbook minimum-norm solution).  Small n only."""
+    least squares (textbook minimum-norm solution).  Small n only.
+
+    Pinned by test_fit_equals_lstsq_minimum_norm (LAPACK minimum-norm least
+    squares)."""
     M = design_matrix(G.shape[0], regions)
     return np.linalg.lstsq(M, G.ravel(), rcond=None)[0]
 
 
 def split_coeffs(X: np.ndarray, n: int):
-    """(c, d, e) views of a coefficient vector."""
+    """(c, d, e) views of a coefficient vector.
+
+    Pinned by test_extrapolation_reproduces_linear_sequences and
+    test_gauge_invariance_of_scores."""
     return X[:2 * n - 1], X[2 * n - 1:3 * n - 1], X[3 * n - 1:]
 
 
 def reconstruct(X: np.ndarray, n: int, regions) -> np.ndarray:
-    """M X as an n x n map: c[j-i] + d[j] + sum of e_f over squares holding (i, j)."""
+    """M X as an n x n map: c[j-i] + d[j] + sum of e_f over squares holding (i, j).
+
+    Pinned by test_planted_coefficients_recovered (M X of a planted X)."""
     c, d, e = split_coeffs(X, n)
     i, j = np.indices((n, n))
     out = c[j - i + n - 1] + d[j]
@@ -289,7 +325,9 @@ def extrapolate(X1: np.ndarray | None, t1: int | None, X2: np.ndarray, t2: int, 
 def gate(e_anchors, tau_e: float) -> bool:
     """Block-diagonal support switch of Section 5.3: kept iff
     min over the warm-up anchors of the frame-averaged e exceeds tau_e.
-    (Reading: the paper's e_min aggregates the per-frame e by their mean.)"""
+    (Reading: the paper's e_min aggregates the per-frame e by their mean.)
+
+    Pinned by test_gate_reading."""
     return bool(min(float(np.mean(e)) for e in e_anchors) > tau_e)
 
 
@@ -301,14 +339,20 @@ def gate(e_anchors, tau_e: float) -> bool:
 def scores(ctil: np.ndarray, dtil: np.ndarray, n: int) -> np.ndarray:
     """sigma(i, j) = n * (c~[j - i] + d~[j]): the predicted diagonal and
     vertical intensities that cover block (i, j) (Section 5.3), scaled by n
-    so that a uniform map scores 1.  Invariant under the gauge X -> X + a z."""
+    so that a uniform map scores 1.  Invariant under the gauge X -> X + a z.
+
+    Pinned by test_gauge_invariance_of_scores and
+    test_pattern_index_convention_picks_the_planted_diagonal_and_column."""
     i, j = np.indices((n, n))
     return n * (ctil[j - i + n - 1] + dtil[j])
 
 
 def forced_mask(n: int, regions, gate_on: bool) -> np.ndarray:
     """K_E: blocks (i, j) that lie in a frame square R_f x R_f, when the gate
-    is on (Section 5.3).  bool [n, n]."""
+    is on (Section 5.3).  bool [n, n].
+
+    Pinned by test_pattern_topk_invariants and
+    test_text_rows_and_columns_full_and_video_part."""
     m = np.zeros((n, n), dtype=bool)
     if gate_on:
         for lo, hi in regions:
@@ -320,7 +364,9 @@ def text_blocks(L_video: int, L: int, bs: int) -> range:
     """Blocks holding at least one text token when a text segment of
     L - L_video tokens follows the video tokens (token-type-aware masking,
     Section 3); empty without text.  A block holding the last video tokens
-    and the first text tokens counts as a text block."""
+    and the first text tokens counts as a text block.
+
+    Pinned by test_text_blocks_layout."""
     if L == L_video:
         return range(0)
     return range(L_video // bs, num_blocks(L, bs))
@@ -332,7 +378,9 @@ def add_text(rows_video, L_video: int, L: int, bs: int):
     blocks keep every block; every other row keeps its video selection plus
     every text block.  rows_video: RowSelection per video query block (the
     selection over the video blocks, the mixed block already forced).
-    Returns one RowSelection per block of the whole sequence."""
+    Returns one RowSelection per block of the whole sequence.
+
+    Pinned by test_text_rows_and_columns_full_and_video_part."""
     n = num_blocks(L, bs)
     tb = text_blocks(L_video, L, bs)
     if len(tb) == 0:
@@ -350,7 +398,9 @@ def add_text(rows_video, L_video: int, L: int, bs: int):
 
 def topk_count(density: float, n: int) -> int:
     """k = clamp(ceil(rho * n), 1, n), with rho taken at float32 precision
-    and a 1e-6 guard so that an integral rho*n is not pushed up by rounding."""
+    and a 1e-6 guard so that an integral rho*n is not pushed up by rounding.
+
+    Pinned by test_topk_count."""
     rho = float(np.float32(density))
     return int(min(n, max(1, math.ceil(rho * n - 1e-6))))
 
@@ -363,12 +413,17 @@ class RowSelection:
 
 
 def _order(keys: np.ndarray, cand: np.ndarray) -> np.ndarray:
-    """Candidates sorted by (key descending, index ascending)."""
+    """Candidates sorted by (key descending, index ascending).
+
+    Pinned by test_selection_ties_break_by_index and test_topk_row_bruteforce."""
     return cand[np.lexsort((cand, -keys[cand]))]
 
 
 def select_row_topk(sig_row: np.ndarray, forced_row: np.ndarray, k: int) -> RowSelection:
-    """Keep the forced blocks plus the k - |F_i| best-scoring others."""
+    """Keep the forced blocks plus the k - |F_i| best-scoring others.
+
+    Pinned by test_topk_row_bruteforce (all subsets of a small row) and
+    test_selection_ties_break_by_index."""
     keys = sig_row.astype(np.float32).astype(np.float64)
     forced = np.flatnonzero(forced_row)
     cand = np.flatnonzero(~forced_row)
@@ -385,7 +440,10 @@ def select_row_topk(sig_row: np.ndarray, forced_row: np.ndarray, k: int) -> RowS
 def select_row_mass(sig_row: np.ndarray, forced_row: np.ndarray, tau: float) -> RowSelection:
     """Keep the forced blocks plus the shortest score-ordered prefix of the
     others whose positive-score mass reaches tau of the row's total
-    (at least one block per row)."""
+    (at least one block per row).
+
+    Pinned by test_mass_row_bruteforce (shortest prefix by brute force) and
+    test_mass_row_zero_mass_keeps_one_block."""
     keys = sig_row.astype(np.float32).astype(np.float64)
     pos = np.maximum(keys, 0.0)
     total = 0.0
@@ -423,7 +481,10 @@ def select_row_mass(sig_row: np.ndarray, forced_row: np.ndarray, tau: float) -> 
 def pattern_values(ctil: np.ndarray, dtil: np.ndarray) -> np.ndarray:
     """The 3n - 1 predicted pattern intensities in pattern order: diagonals
     delta = -(n-1) .. n-1 (index delta + n - 1), then columns j (index
-    2n - 1 + j)."""
+    2n - 1 + j).
+
+    Pinned by test_pattern_topk_bruteforce and
+    test_pattern_topk_planted_diagonal_and_column."""
     return np.concatenate([np.asarray(ctil, dtype=np.float64), np.asarray(dtil, dtype=np.float64)])
 
 
@@ -436,7 +497,12 @@ def select_patterns(ctil: np.ndarray, dtil: np.ndarray, n: int, K: int, forced: 
     ranking depends on the gauge of (c, d); the minimum-norm solution is
     used.  Rows that no kept pattern reaches keep nothing.  Returns one
     RowSelection per query block; key_gap is the head's boundary gap (the
-    K-th minus the (K+1)-th key, inf when K covers every pattern)."""
+    K-th minus the (K+1)-th key, inf when K covers every pattern).
+
+    Pinned by test_pattern_topk_bruteforce,
+    test_pattern_topk_planted_diagonal_and_column,
+    test_pattern_topk_all_patterns_keep_every_block_and_ties and
+    test_pattern_topk_invariants."""
     vals = pattern_values(ctil, dtil).astype(np.float32).astype(np.float64)
     P = vals.size
     K = int(min(P, max(1, K)))
@@ -453,7 +519,11 @@ def select_patterns(ctil: np.ndarray, dtil: np.ndarray, n: int, K: int, forced: 
 def select(sig: np.ndarray, forced: np.ndarray, mode: str, density: float = 1.0,
            mass: float = 1.0):
     """Per-row selection over an n x n score map.  Returns a list of
-    RowSelection, one per query block."""
+    RowSelection, one per query block.
+
+    Pinned by
+    test_pattern_index_convention_picks_the_planted_diagonal_and_column and
+    test_text_rows_and_columns_full_and_video_part."""
     n = sig.shape[0]
     if mode == "topk":
         k = topk_count(density, n)
@@ -698,6 +768,10 @@ def attention_statistic(q: np.ndarray, k: np.ndarray, kept_lists, bs: int, scale
     may round the decision differently).  rows: optional subset of query
     blocks (the other rows stay NaN / 0).  return_lse: also return the row
     LSE used ([L], NaN outside ``rows``).
+
+    Pinned by test_attention_statistic_bruteforce (entry by entry from the
+    dense attention) and
+    test_attention_statistic_uniform_attention_closed_form.
     """
     L = q.shape[0]
     n = num_blocks(L, bs)
@@ -733,7 +807,9 @@ def reconstruct_statistic(history: np.ndarray | None, current: np.ndarray) -> np
     """Eq. 5 at block level: entries computed at this step (finite in
     ``current``) replace the history; blocks the mask dropped keep their
     historical value.  The first map must be dense (Algorithm 1 starts the
-    sequence from the full attention of the warm-up)."""
+    sequence from the full attention of the warm-up).
+
+    Pinned by test_reconstruction_keeps_dropped_blocks."""
     if history is None:
         if np.isnan(current).any():
             raise ValueError("the first statistic must cover every block (dense step)")
@@ -753,14 +829,20 @@ def paper_op_counts(N: int, H: int, d: int, p: int):
     """Operation counts in the units of the paper's Appendix C table:
     full attention 2 N^2 d H, conversion to the sparsity map N^2 H (one
     compare per attention entry), dense solve p^3 / 3 (one Cholesky of the
-    p x p normal matrix).  Returned in TFLOP."""
+    p x p normal matrix).  Returned in TFLOP.
+
+    Pinned by test_flop_table_matches_paper (the values printed in the
+    Appendix C table, tests/golden/paper_flop_table.json)."""
     return 2.0 * N * N * d * H / 1e12, 1.0 * N * N * H / 1e12, p ** 3 / 3.0 / 1e12
 
 
 def kept_block_flops(kept_lists, L: int, bs: int, d: int) -> float:
     """4 d sum over kept (i, j) of |i| |j|: QK^T and PV multiply-adds counted
     as 2 flops each, valid tokens only.  kept_lists: iterable over heads of
-    per-row lists."""
+    per-row lists.
+
+    Pinned by test_kept_block_flops_full_mask_is_dense_count (4 d L^2 for a
+    full mask)."""
     sizes = block_sizes(L, bs)
     tot = 0
     for rows in kept_lists:
