@@ -1308,14 +1308,17 @@ hipError_t launch(const uint16_t* q, const uint16_t* k, const uint16_t* v, const
 // block (i, j), the fraction of the probabilities exp(scale q_p.k_q - LSE_p)
 // that reach eta, LSE_p being the row LSE the attention forward returned
 // over the same lists (the masked map; all blocks at a dense step).  The
-// decision is taken in fp32 as s >= (LSE_p + log(eta)) / scale, s the fp32
-// MFMA product.  Like the attention, one work-group per (head, pair of query
+// decision is taken in fp32 as s - thr >= 0, thr = (LSE_p + log(eta)) /
+// scale, s - thr accumulated by the MFMA products from -thr (it differs
+// from rounding s first by a few ulps of s, far inside the log-space band
+// where an fp64 reference and any fp32 evaluation may disagree).  Like the
+// attention, one work-group per (head, pair of query
 // blocks 2p, 2p+1) walks the union of the two lists with two groups of BS/32
 // waves (32 query rows each), so every K tile copied into LDS serves both
 // blocks (double-buffered, every wave copying its share of the next tile).
 // Per tile each wave computes S^T = K Q^T for its 32 query rows by MFMA and
-// counts its entries that reach the row's threshold (one 64-lane compare
-// mask per score, counted and summed on the scalar unit).  The groups are
+// counts its entries that reach the row's threshold (the sign bits of the
+// lane's values summed per lane, then over the wave).  The groups are
 // skewed by one tile with a single work-group barrier per tile: in the
 // interval of tile t group 0 multiplies tile t and then counts it, while
 // group 1 first counts tile t-1 (its scores kept in registers) and then
@@ -1379,7 +1382,12 @@ __global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
     const int ka = l32 * ROWB + ((h ^ swz<D>(l32)) << 4);
 
     f32x16 sacc[RT];
-    // S^T of a whole tile: the RT sub-tiles' chains interleaved, operand
+    // the products start from -thr, so a score reaches the threshold iff
+    // its accumulated value is not negative
+    f32x16 nthr;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) nthr[e] = -thr;
+    // S^T - thr of a whole tile: the RT sub-tiles' chains interleaved, operand
     // loads PF steps ahead of their products (pinned step by step)
     auto multiply = [&](const char* kt) __attribute__((always_inline)) {
         constexpr int NS = RT * KK;
@@ -1396,7 +1404,7 @@ __global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
         for (int s2 = 0; s2 < NS; ++s2) {
             if (s2 + PF < NS) load(s2 + PF);
             const int kk = s2 / RT, rt = s2 % RT;
-            sacc[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[s2], qreg[kk], kk == 0 ? f32x16{} : sacc[rt], 0, 0,
+            sacc[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[s2], qreg[kk], kk == 0 ? nthr : sacc[rt], 0, 0,
                                                                0);
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -1415,35 +1423,26 @@ __global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
                     sacc[rt][ii] = (8 * (ii >> 2) + (ii & 3) >= lim) ? -INFINITY : sacc[rt][ii];
             }
         }
-        // the wave's count: one compare mask per score (64 lanes), counted
-        // and summed on the scalar unit, four scores per block
-        int c = 0;
+        // the lane's count: the sign bits of its 16 RT values (S - thr; -inf
+        // for the masked rows) summed two at a time into three-input
+        // additions, subtracted from the number of values; then the wave's
+        // sum: within each row of 16 lanes by DPP, over the four rows on the
+        // scalar unit
+        uint32_t n0 = 0, n1 = 0;
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
             for (int ii = 0; ii < 16; ii += 4) {
-                uint64_t m0, m1, m2, m3;
-                int b0, b1;
-                asm volatile(
-                    "v_cmp_ge_f32_e64 %[m0], %[x0], %[t]\n\t"
-                    "v_cmp_ge_f32_e64 %[m1], %[x1], %[t]\n\t"
-                    "v_cmp_ge_f32_e64 %[m2], %[x2], %[t]\n\t"
-                    "v_cmp_ge_f32_e64 %[m3], %[x3], %[t]\n\t"
-                    "s_nop 3\n\t"
-                    "s_bcnt1_i32_b64 %[b0], %[m0]\n\t"
-                    "s_bcnt1_i32_b64 %[b1], %[m1]\n\t"
-                    "s_add_u32 %[c], %[c], %[b0]\n\t"
-                    "s_bcnt1_i32_b64 %[b0], %[m2]\n\t"
-                    "s_add_u32 %[c], %[c], %[b1]\n\t"
-                    "s_bcnt1_i32_b64 %[b1], %[m3]\n\t"
-                    "s_add_u32 %[c], %[c], %[b0]\n\t"
-                    "s_add_u32 %[c], %[c], %[b1]"
-                    : [c] "+s"(c), [m0] "=&s"(m0), [m1] "=&s"(m1), [m2] "=&s"(m2), [m3] "=&s"(m3),
-                      [b0] "=&s"(b0), [b1] "=&s"(b1)
-                    : [x0] "v"(sacc[rt][ii]), [x1] "v"(sacc[rt][ii + 1]), [x2] "v"(sacc[rt][ii + 2]),
-                      [x3] "v"(sacc[rt][ii + 3]), [t] "v"(thr)
-                    : "scc");
+                n0 += (__float_as_uint(sacc[rt][ii]) >> 31) + (__float_as_uint(sacc[rt][ii + 1]) >> 31);
+                n1 += (__float_as_uint(sacc[rt][ii + 2]) >> 31) + (__float_as_uint(sacc[rt][ii + 3]) >> 31);
             }
+        int v = (int)(16u * RT - n0 - n1);
+        v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);    // quad_perm [1,0,3,2]
+        v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);    // quad_perm [2,3,0,1]
+        v += __builtin_amdgcn_update_dpp(0, v, 0x124, 0xF, 0xF, false);   // row_ror:4
+        v += __builtin_amdgcn_update_dpp(0, v, 0x128, 0xF, 0xF, false);   // row_ror:8
+        const int c = __builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 16) +
+                      __builtin_amdgcn_readlane(v, 32) + __builtin_amdgcn_readlane(v, 48);
         return c;   // the wave's count
     };
     // group gg's count of a finished tile (block 2p+gg, kv block j)
