@@ -882,12 +882,13 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     // addresses of the K operand (32-row slice rt, d-chunk kk) and of the
     // two halves of the V^T operand (16 kv rows cc, d-tile dt).  The two
     // products are independent and interleaved; operand reads run PF steps
-    // ahead of their products.
+    // ahead of their products (one step: with no address arithmetic in the
+    // phase, two or three steps ran 0.5% and 1.1% slower).
     auto mphase_at = [&](auto&& kp, auto&& vp) __attribute__((always_inline)) {
         // the matrix phase issues first when both waves of a SIMD are ready
         __builtin_amdgcn_s_setprio(1);
         constexpr int NS = RT * KK;
-        constexpr int PF = 2;
+        constexpr int PF = 1;
         bf16x8 ak[NS];
         s16x4 va4[NS], vb4[NS];
         auto load = [&](auto si) __attribute__((always_inline)) {
