@@ -120,13 +120,22 @@ def parse():
     return ap.parse_args()
 
 
-def source_digest(path: str = ATTN_SOURCE) -> str:
-    """Digest of a kernel source's code: comments dropped (string and
-    character literals kept as written) and whitespace runs collapsed, so
-    that an edit of the comments alone leaves it unchanged."""
+# The attention source also holds the Eq. 2 count kernel after this banner;
+# the attention's digest covers the text before it (the helpers, the work
+# plan, the merge, the attention kernel and its launch).
+ATTN_SECTION_END = "// Eq. 2 statistic of the attention map"
+
+
+def source_digest(path: str = ATTN_SOURCE, upto: str | None = ATTN_SECTION_END) -> str:
+    """Digest of a kernel source's code (the text before ``upto`` when the
+    source holds it): comments dropped (string and character literals kept
+    as written) and whitespace runs collapsed, so that an edit of the
+    comments alone leaves it unchanged."""
     import hashlib
     with open(path, encoding="utf-8") as f:
         text = f.read()
+    if upto is not None and upto in text:
+        text = text[:text.index(upto)]
     out, i, n = [], 0, len(text)
     while i < n:
         c = text[i]
