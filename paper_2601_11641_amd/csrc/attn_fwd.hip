@@ -1427,27 +1427,34 @@ __global__ __launch_bounds__(BS * 4, 1) void stat_count_kernel(
                     sacc[rt][ii] = (8 * (ii >> 2) + (ii & 3) >= lim) ? -INFINITY : sacc[rt][ii];
             }
         }
-        // the lane's count: the sign bits of its 16 RT values (S - thr; -inf
-        // for the masked rows) summed two at a time into three-input
-        // additions, subtracted from the number of values; then the wave's
-        // sum: within each row of 16 lanes by DPP, over the four rows on the
-        // scalar unit
-        uint32_t n0 = 0, n1 = 0;
+        // the lane's count from the sign bits of its 16 RT values (S - thr;
+        // -inf for the masked rows): one byte permute per two values turns
+        // the sign bit of the first into 0xFF or 0 in byte 2 and that of the
+        // second in byte 0 (selectors 11 and 9 replicate bit 31 of the first
+        // and second source), and three-input additions sum two permutes at
+        // a time, so each 16-bit half of acc holds 255 x (a count of at most
+        // 8 RT) and no carry crosses between them: 0.75 vector instructions
+        // per value.  Then the wave's sum, still scaled by 255: within each
+        // row of 16 lanes by DPP, over the four rows on the scalar unit.
+        uint32_t acc = 0;
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
             for (int ii = 0; ii < 16; ii += 4) {
-                n0 += (__float_as_uint(sacc[rt][ii]) >> 31) + (__float_as_uint(sacc[rt][ii + 1]) >> 31);
-                n1 += (__float_as_uint(sacc[rt][ii + 2]) >> 31) + (__float_as_uint(sacc[rt][ii + 3]) >> 31);
+                const uint32_t p0 = __builtin_amdgcn_perm(__float_as_uint(sacc[rt][ii]),
+                                                          __float_as_uint(sacc[rt][ii + 1]), 0x0C0B0C09u);
+                const uint32_t p1 = __builtin_amdgcn_perm(__float_as_uint(sacc[rt][ii + 2]),
+                                                          __float_as_uint(sacc[rt][ii + 3]), 0x0C0B0C09u);
+                acc += p0 + p1;
             }
-        int v = (int)(16u * RT - n0 - n1);
+        int v = (int)(255u * 16u * RT - ((acc & 0xFFFFu) + (acc >> 16)));
         v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);    // quad_perm [1,0,3,2]
         v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);    // quad_perm [2,3,0,1]
         v += __builtin_amdgcn_update_dpp(0, v, 0x124, 0xF, 0xF, false);   // row_ror:4
         v += __builtin_amdgcn_update_dpp(0, v, 0x128, 0xF, 0xF, false);   // row_ror:8
         const int c = __builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 16) +
                       __builtin_amdgcn_readlane(v, 32) + __builtin_amdgcn_readlane(v, 48);
-        return c;   // the wave's count
+        return (int)((uint32_t)c / 255u);   // the wave's count
     };
     // group gg's count of a finished tile (block 2p+gg, kv block j)
     auto flush = [&](int gg, int parity, int j) __attribute__((always_inline)) {
