@@ -536,15 +536,17 @@ __global__ __launch_bounds__(kThreads) void extrapolate_kernel(const double* __r
 
 // ---------------------------------------------------------------------------
 // a5: per-row selection.  One wave per (head, query block i) up to n = 1024
-// (select_wave_kernel), one work-group of 256 threads per row above.
+// (select_wave_kernel, a threshold search), one work-group of 256 threads per
+// row above (select_kernel, a sort).
 //   sigma_j = n (c~[j-i] + d~[j]) in fp64, rounded to float: the ranking key.
-//   Non-forced blocks get the 64-bit key (order(sigma) << 32 | ~j), so one
-//   descending bitonic sort orders them by (sigma desc, j asc); forced blocks
-//   and padding get key 0 and sort last.
-//   TOPK keeps the first max(0, k - |forced|) sorted blocks; MASS keeps the
-//   shortest prefix whose positive key mass, added to the forced blocks'
-//   mass, reaches tau of the row total (fp64 prefix sums; at least one block).
-//   The kept set is compacted in ascending j.
+//   The non-forced blocks are ranked by (sigma desc, j asc).  TOPK keeps the
+//   first max(0, k - |forced|) of them; MASS keeps the shortest prefix whose
+//   positive key mass, added to the forced blocks' mass, reaches tau of the
+//   row total (fp64 sums; at least one block).  The kept set is compacted in
+//   ascending j.
+//   select_kernel gives every non-forced block the 64-bit key
+//   (order(sigma) << 32 | ~j) and sorts descending (bitonic), forced blocks
+//   and padding with key 0 last, and takes prefix sums in sorted order.
 // With a text segment after the video (token-type-aware masking) n counts
 // the video blocks, the lists have ldn >= n entries per row, the block tb0
 // shared by the video and the text (tb0 < n) is forced, and every row keeps
@@ -752,27 +754,6 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
 }
 
 
-// The same selection with one wave per row (n <= 64 * EW): the row's keys in
-// registers, EW per lane (lane l holds positions EW*l .. EW*l+EW-1 of the
-// sort, starting with the keys of blocks l + 64 e: coalesced loads), every
-// stage of the sort, the forced-mass sum, the mass prefix, the choice of
-// the kept count and the compaction across the wave's lanes, so no
-// work-group barrier is needed; a wave's flags live in its own LDS bytes.
-// Four waves (rows) per work-group.
-__device__ inline double wave_sum_f64(double v) {
-    // butterfly: partners add the same two values, so every lane ends with
-    // the same bits (a fixed order)
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    return v;
-}
-
-__device__ inline int wave_min_i32(int v) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v = min(v, __shfl_xor(v, off));
-    return v;
-}
-
 template <class T>
 __device__ inline T wave_inclusive_scan(T v, int lane) {
 #pragma unroll
@@ -788,52 +769,52 @@ __device__ inline void wave_sync_lds() {
     __builtin_amdgcn_wave_barrier();
 }
 
-// Stage (KK, JJ) of a descending bitonic sort over the 64*EW keys of a wave
-// (lane l holds positions EW*l .. EW*l+EW-1): positions a and a ^ JJ are
-// compared, the lower one keeps the larger key when (a & KK) == 0.  The
-// stages are template arguments so that every exchange is resolved at
-// compile time (an unrolled loop over them exceeds the unroller's budget).
-template <int EW, int KK, int JJ>
-__device__ __forceinline__ void bitonic_stage_wave(uint64_t (&kr)[EW], int lane) {
-    if constexpr (JJ < EW) {
-#pragma unroll
-        for (int e = 0; e < EW; ++e) {
-            const int eb = e ^ JJ;
-            if (eb > e) {
-                const int a = EW * lane + e;
-                const bool desc = (a & KK) == 0;
-                const uint64_t ka = kr[e], kb = kr[eb];
-                const bool swap = desc ? (ka < kb) : (ka > kb);
-                kr[e] = swap ? kb : ka;
-                kr[eb] = swap ? ka : kb;
-            }
-        }
-    } else {
-#pragma unroll
-        for (int e = 0; e < EW; ++e) {
-            const uint64_t pv = shfl_xor_u64<true>(kr[e], JJ / EW);
-            const int a = EW * lane + e;
-            const bool lower = (a & JJ) == 0;
-            const bool desc = (a & KK) == 0;
-            const uint64_t hi = kr[e] > pv ? kr[e] : pv;
-            const uint64_t lo = kr[e] > pv ? pv : kr[e];
-            kr[e] = (lower == desc) ? hi : lo;
-        }
+// The wave's total of a per-lane double in a fixed order, the same bits in
+// every lane: sums within rows of 16 lanes by DPP (lane pairs, quad pairs,
+// then rotations by 4 and 8, after which lane 0 of a row holds its row's
+// sum), then the four row sums read from lanes 0, 16, 32 and 48.
+__device__ inline double dpp_f64(double v, int ctrl_id) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    uint32_t lo = static_cast<uint32_t>(u), hi = static_cast<uint32_t>(u >> 32);
+    switch (ctrl_id) {
+        case 0: lo = __builtin_amdgcn_mov_dpp((int)lo, 0xB1, 0xF, 0xF, false);
+                hi = __builtin_amdgcn_mov_dpp((int)hi, 0xB1, 0xF, 0xF, false); break;   // quad_perm 1,0,3,2
+        case 1: lo = __builtin_amdgcn_mov_dpp((int)lo, 0x4E, 0xF, 0xF, false);
+                hi = __builtin_amdgcn_mov_dpp((int)hi, 0x4E, 0xF, 0xF, false); break;   // quad_perm 2,3,0,1
+        case 2: lo = __builtin_amdgcn_mov_dpp((int)lo, 0x124, 0xF, 0xF, false);
+                hi = __builtin_amdgcn_mov_dpp((int)hi, 0x124, 0xF, 0xF, false); break;  // row_ror:4
+        default: lo = __builtin_amdgcn_mov_dpp((int)lo, 0x128, 0xF, 0xF, false);
+                 hi = __builtin_amdgcn_mov_dpp((int)hi, 0x128, 0xF, 0xF, false); break; // row_ror:8
     }
+    return __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
 }
 
-template <int EW, int KK, int JJ>
-__device__ __forceinline__ void bitonic_merge_wave(uint64_t (&kr)[EW], int lane) {
-    bitonic_stage_wave<EW, KK, JJ>(kr, lane);
-    if constexpr (JJ > 1) bitonic_merge_wave<EW, KK, JJ / 2>(kr, lane);
+__device__ inline double readlane_f64(double v, int l) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(u), l);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(u >> 32), l);
+    return __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
 }
 
-template <int EW, int KK>
-__device__ __forceinline__ void bitonic_sort_wave(uint64_t (&kr)[EW], int lane) {
-    bitonic_merge_wave<EW, KK, KK / 2>(kr, lane);
-    if constexpr (KK < 64 * EW) bitonic_sort_wave<EW, 2 * KK>(kr, lane);
+__device__ inline double wave_total_f64(double v) {
+    v += dpp_f64(v, 0);
+    v += dpp_f64(v, 1);
+    v += dpp_f64(v, 2);
+    v += dpp_f64(v, 3);
+    return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
 }
 
+// One wave per row (n <= 64 EW).  Every free block j holds its ranking key
+// as the order bits of sigma_j (vb, 0 for forced blocks and padding) and its
+// positive mass.  The kept free blocks are those whose bits exceed a
+// boundary p, plus the first r in ascending j of those whose bits equal p:
+// the same set as the first keep entries of the (sigma desc, j asc) order.
+//   TOPK: p is the largest 32-bit value with at least keep free keys at or
+//     above it (built bit by bit from the top, 32 wave-wide counts).
+//   MASS: p is the largest value whose keys at or above it, added to the
+//     forced mass, reach tau of the row total (32 fixed-order fp64 wave
+//     sums); every key above p is needed, and r is the fewest keys at p
+//     (all of mass max(sigma_p, 0)) that reach the target with them.
 template <int EW>
 __global__ __launch_bounds__(kThreads) void select_wave_kernel(
     const double* __restrict__ pred, const int32_t* __restrict__ gate,
@@ -859,11 +840,13 @@ __global__ __launch_bounds__(kThreads) void select_wave_kernel(
     const int n_free = n - nf;
 
     double forced_mass = 0.0;
-    uint64_t kr[EW];
+    uint32_t vb[EW];
+    double ms[EW];
 #pragma unroll
     for (int e = 0; e < EW; ++e) {
-        const int j = lane + 64 * e;   // coalesced; the sort places keys by value
-        uint64_t key = 0;
+        const int j = lane + 64 * e;   // coalesced
+        vb[e] = 0;
+        ms[e] = 0.0;
         uint8_t fl = 0;
         if (j < n) {
             const double sv = static_cast<double>(n) * (c[j - i + n - 1] + d[j]);
@@ -872,64 +855,101 @@ __global__ __launch_bounds__(kThreads) void select_wave_kernel(
                 fl = 1;
                 forced_mass += fmax(static_cast<double>(kf), 0.0);
             } else {
-                key = (static_cast<uint64_t>(order_bits(kf)) << 32) |
-                      static_cast<uint64_t>(0xFFFFFFFFu - static_cast<uint32_t>(j));
+                vb[e] = order_bits(kf);
+                ms[e] = fmax(static_cast<double>(kf), 0.0);
             }
         }
-        kr[e] = key;
         flag[j] = fl;
     }
+    auto count_ge = [&](uint32_t th) {   // free keys with bits >= th (th >= 1)
+        int cnt = 0;
+#pragma unroll
+        for (int e = 0; e < EW; ++e) cnt += __popcll(__ballot(vb[e] >= th));
+        return cnt;
+    };
+    auto mass_ge = [&](uint32_t th) {    // their mass (th >= 1)
+        double s = 0.0;
+#pragma unroll
+        for (int e = 0; e < EW; ++e) s += vb[e] >= th ? ms[e] : 0.0;
+        return wave_total_f64(s);
+    };
+    // largest p with count_ge(p) >= kk (kk >= 1, at most n_free)
+    auto kth_bits = [&](int kk) {
+        uint32_t p = 0;
+        for (int b = 31; b >= 0; --b) {
+            const uint32_t th = p | (1u << b);
+            if (count_ge(th) >= kk) p = th;
+        }
+        return p;
+    };
 
-    // descending bitonic sort of the npad keys (stages as in select_kernel;
-    // partners in other lanes are exchanged across the wave)
-    bitonic_sort_wave<EW, 2>(kr, lane);
-
-    int keep;
+    uint32_t p;   // boundary bits
+    int r;        // keys kept at the boundary, in ascending j
+    int keep = -1;  // free keys kept when all or none are
     if (mode == 0) {
         keep = min(n_free, max(0, topk - nf));
     } else {
-        const double fm = wave_sum_f64(forced_mass);
-        // inclusive prefix of the positive masses in sorted order: within the
-        // lane, then the lanes' totals scanned across the wave
-        double part[EW];
-        double run = 0.0;
-#pragma unroll
-        for (int e = 0; e < EW; ++e) {
-            const int pos = EW * lane + e;
-            const double v =
-                pos < n_free
-                    ? fmax(static_cast<double>(order_bits_to_float(static_cast<uint32_t>(kr[e] >> 32))), 0.0)
-                    : 0.0;
-            run += v;
-            part[e] = run;
-        }
-        const double incl = wave_inclusive_scan(run, lane);
-        const double base = incl - run;                 // positions before this lane
-        const double all = __shfl(incl, 63);
-        const double target = tau * (fm + all);
+        const double fm = wave_total_f64(forced_mass);
+        const double total = fm + (n_free > 0 ? mass_ge(1u) : 0.0);
+        const double target = tau * total;
         const int kmin = nf > 0 ? 0 : 1;
-        // keeping `cand` free blocks reaches fm + (mass of positions < cand)
-        int best = n_free;
-#pragma unroll
-        for (int e = EW - 1; e >= 0; --e) {
-            const int cand = EW * lane + e;
-            if (cand < kmin || cand > n_free) continue;
-            const double before = cand == 0 ? 0.0 : (e == 0 ? base : base + part[e - 1]);
-            if (fm + before >= target) best = cand;
+        if (fm >= target) {
+            keep = min(n_free, kmin);
+        } else if (total < target) {
+            keep = n_free;
+        } else {
+            // the boundary key has a positive mass, so its sign bit is set
+            // (every non-negative key's mass is the total's free part)
+            p = 0x80000000u;
+            for (int b = 30; b >= 0; --b) {
+                const uint32_t th = p | (1u << b);
+                if (fm + mass_ge(th) >= target) p = th;
+            }
+            const double hi = fm + (p < 0xFFFFFFFFu ? mass_ge(p + 1) : 0.0);
+            const int ties = count_ge(p) - (p < 0xFFFFFFFFu ? count_ge(p + 1) : 0);
+            const double mp = fmax(static_cast<double>(order_bits_to_float(p)), 0.0);
+            r = 1;
+            while (r < ties && hi + static_cast<double>(r) * mp < target) ++r;
         }
-        keep = wave_min_i32(best);
     }
-    wave_sync_lds();
+    if (keep >= 0) {
+        if (keep == 0) {
+            p = 0xFFFFFFFFu;
+            r = 0;
+        } else if (keep >= n_free) {
+            p = 0;
+            r = 0;
+        } else {
+            p = kth_bits(keep);
+            r = keep - (p < 0xFFFFFFFFu ? count_ge(p + 1) : 0);
+        }
+    }
+    // flags: 1 kept, 2 at the boundary (resolved below in ascending j)
 #pragma unroll
     for (int e = 0; e < EW; ++e) {
-        if (EW * lane + e < keep) flag[0xFFFFFFFFu - static_cast<uint32_t>(kr[e] & 0xFFFFFFFFull)] = 1;
+        const int j = lane + 64 * e;
+        if (vb[e] > p)
+            flag[j] = 1;
+        else if (vb[e] == p && vb[e] != 0)
+            flag[j] = 2;
     }
     wave_sync_lds();
-
-    // compaction in ascending j
+    uint8_t f[EW];
+    int nt = 0;
+#pragma unroll
+    for (int e = 0; e < EW; ++e) {
+        f[e] = flag[EW * lane + e];
+        nt += f[e] == 2;
+    }
+    int tr = wave_inclusive_scan(nt, lane) - nt;   // boundary keys before this lane
     int cnt = 0;
 #pragma unroll
-    for (int e = 0; e < EW; ++e) cnt += flag[EW * lane + e];
+    for (int e = 0; e < EW; ++e) {
+        if (f[e] == 2) f[e] = tr++ < r ? 1 : 0;
+        cnt += f[e];
+    }
+
+    // compaction in ascending j
     const int incl_c = wave_inclusive_scan(cnt, lane);
     int pos = incl_c - cnt;
     const int total = __shfl(incl_c, 63);
@@ -938,7 +958,7 @@ __global__ __launch_bounds__(kThreads) void select_wave_kernel(
 #pragma unroll
     for (int e = 0; e < EW; ++e) {
         const int j = EW * lane + e;
-        if (flag[j]) out[pos++] = j;
+        if (f[e]) out[pos++] = j;
     }
     for (int j = n + lane; j < ldn; j += 64) out[total + (j - n)] = j;
     if (lane == 0) kv_cnt[orow] = total + (ldn - n);
