@@ -219,6 +219,40 @@ def test_ragged_shapes(name, budget):
     st.close()
 
 
+@pytest.mark.parametrize("name", ["ragged128", "d64b64"])
+@pytest.mark.parametrize("budget", [("topk", 0.4), ("mass", 0.7)])
+@pytest.mark.parametrize("tau_e", [-1.0, 1.0])
+def test_tied_scores(name, budget, tau_e):
+    """Every token of Q, and every token of K, the same vector: all pooled
+    block logits of a head are equal, so the scores of a row tie (one or two
+    distinct float32 keys: the short tail block's differs) and the lists rest
+    on the tie rule of the per-row ranking (equal keys in ascending j), which
+    the GPU must reproduce row for row.  The frame energy of such a map is
+    zero up to rounding, so the gate threshold is set clearly below it
+    (frame blocks forced) or above it (none forced)."""
+    cfg = RAGGED[name]
+    q, k, v = W.generate(cfg)
+    q = np.ascontiguousarray(np.broadcast_to(q[:, :, :1, :], q.shape))
+    k = np.ascontiguousarray(np.broadcast_to(k[:, :, :1, :], k.shape))
+    host = (q, k, v)
+    dev = tuple(bf16_tensor(x) for x in host)
+    params = dict(warmup_m=1, delta_t=0, tau_e=tau_e)
+    st, kv_idx, kv_cnt, P, sel, qf, kf = _run_predictor(cfg, dev, host, [1], 2, budget, params)
+    assert P.gates.all() == (tau_e < 0) and P.gates.any() == (tau_e < 0)
+    po = P.prediction(2)
+    ct, dt_ = po[0][0]
+    keys = O.scores(ct, dt_, st.n).astype(np.float32)
+    assert max(len(set(r.tolist())) for r in keys) <= 2      # the ties are there
+    rows = gpu_lists(kv_idx, kv_cnt)
+    for b in range(cfg.B):
+        for h in range(cfg.H):
+            for i in range(st.n):
+                assert rows[b][h][i] == sel[b][h][i].kept.tolist(), (b, h, i)
+    _check_predictor(cfg, st, kv_idx, kv_cnt, P, sel, qf, kf, budget, 2)
+    _check_attention(cfg, dev, host, rows)
+    st.close()
+
+
 @pytest.mark.parametrize("K", [1, 5, 12, 47])
 def test_tiny_pattern_mode(K):
     """Pattern-level Top-K (K of the 3n-1 = 47 patterns; 47 keeps all)."""
