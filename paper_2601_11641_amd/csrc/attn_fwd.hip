@@ -883,7 +883,8 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
     // two halves of the V^T operand (16 kv rows cc, d-tile dt).  The two
     // products are independent and interleaved; operand reads run PF steps
     // ahead of their products (one step: with no address arithmetic in the
-    // phase, two or three steps ran 0.5% and 1.1% slower).
+    // phase, two or three steps ran 0.5% and 1.1% slower, and two steps
+    // 0.35% slower with the reads between the products).
     auto mphase_at = [&](auto&& kp, auto&& vp) __attribute__((always_inline)) {
         // the matrix phase issues first when both waves of a SIMD are ready
         __builtin_amdgcn_s_setprio(1);
@@ -901,10 +902,13 @@ __global__ __launch_bounds__(BS * 4, 1) void attn_fwd_kernel(
         static_for<PF>(load);
         static_for<NS>([&](auto si) __attribute__((always_inline)) {
             constexpr int s = decltype(si)::value;
-            if constexpr (s + PF < NS) load(std::integral_constant<int, s + PF>{});
             constexpr int rt = s / KK, kk = s % KK, cc = s / DT, dt = s % DT;
             sacc[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[s], qreg[kk], kk == 0 ? f32x16{} : sacc[rt], 0, 0,
                                                                0);
+            // the next step's operand reads go out between this step's two
+            // products (before the S^T product 0.3% slower, split around
+            // the PV product 1% slower)
+            if constexpr (s + PF < NS) load(std::integral_constant<int, s + PF>{});
             __builtin_amdgcn_sched_barrier(0);
             const s16x8 v8 = {va4[s][0], va4[s][1], va4[s][2], va4[s][3],
                               vb4[s][0], vb4[s][1], vb4[s][2], vb4[s][3]};
