@@ -812,8 +812,9 @@ __device__ inline double wave_total_f64(double v) {
 //   TOPK: p is the largest 32-bit value with at least keep free keys at or
 //     above it (built bit by bit from the top, 32 wave-wide counts).
 //   MASS: p is the largest value whose keys at or above it, added to the
-//     forced mass, reach tau of the row total (32 fixed-order fp64 wave
-//     sums); every key above p is needed, and r is the fewest keys at p
+//     forced mass, reach tau of the row total (31 fixed-order fp64 wave
+//     sums below the sign bit, which a key of positive mass has set); every
+//     key above p is needed, and r is the fewest keys at p
 //     (all of mass max(sigma_p, 0)) that reach the target with them.
 template <int EW>
 __global__ __launch_bounds__(kThreads) void select_wave_kernel(
