@@ -302,27 +302,37 @@ __device__ __forceinline__ int clamp_count(const int32_t* kv_cnt, size_t row, in
     return min(max(kv_cnt[row], 0), n);
 }
 
-// Work-group sums and exclusive scans over kPlanThreads threads.
+// Work-group sums and exclusive scans over kPlanThreads threads: a scan
+// within each wave by lane shuffles, the waves' totals through buf (at least
+// kPlanThreads / 64 entries), two barriers.
 template <class T>
 __device__ T plan_scan(T v, T* buf, T& total) {
-    const int t = threadIdx.x;
-    buf[t] = v;
-    __syncthreads();
-    for (int off = 1; off < kPlanThreads; off <<= 1) {
-        const T y = t >= off ? buf[t - off] : T(0);
-        __syncthreads();
-        buf[t] += y;
-        __syncthreads();
+    constexpr int NW = kPlanThreads / 64;
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    T incl = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const T y = __shfl_up(incl, off);
+        if (lane >= off) incl += y;
     }
-    total = buf[kPlanThreads - 1];
-    const T ex = buf[t] - v;
+    if (lane == 63) buf[w] = incl;
     __syncthreads();
-    return ex;
+    T base = T(0), tot = T(0);
+#pragma unroll
+    for (int ww = 0; ww < NW; ++ww) {
+        const T s = buf[ww];
+        base += ww < w ? s : T(0);
+        tot += s;
+    }
+    total = tot;
+    __syncthreads();   // buf is free for the next scan
+    return base + incl - v;
 }
 
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const int32_t* __restrict__ kv_cnt, void* ws,
                                                             int BH, int n, int ncu, int S) {
-    __shared__ long long scan64[kPlanThreads];
+    __shared__ long long scan64[kPlanThreads / 64];
+    __shared__ int scan32[kPlanThreads / 64];
     __shared__ int xcnt[kXcds];
     __shared__ uint32_t cache[kPlanCache];   // both counts of a pair, 16 bits each
     const int x = blockIdx.x, t = threadIdx.x;
@@ -338,13 +348,32 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const int32_t* __res
         const size_t r0 = (size_t)bh * n + 2 * p;
         return Pair{clamp_count(kv_cnt, r0, n), 2 * p + 1 < n ? clamp_count(kv_cnt, r0 + 1, n) : 0};
     };
+    // head and pair index of q0, advanced pair by pair in the loops below
+    // (no division per pair)
+    const int h0 = (int)(q0 / npairs), p0 = (int)(q0 % npairs);
     // every pass reads the counts: from LDS when they fit (loaded once,
     // coalesced), else from the lists' counts in memory
     const bool cached = P <= kPlanCache;
     if (cached) {
-        for (long long q = t; q < P; q += kPlanThreads) {
-            const Pair c = load_counts(q);
-            cache[q] = (uint32_t)c.c0 | ((uint32_t)c.c1 << 16);
+        // every thread's loads issued at once (indices clamped to the last
+        // pair, so that no load sits behind a branch), then stored
+        constexpr int FILL = kPlanCache / kPlanThreads;
+        const int Pi = (int)P;
+        int c0[FILL], c1[FILL];
+#pragma unroll
+        for (int u = 0; u < FILL; ++u) {
+            const int q = min(t + u * kPlanThreads, Pi - 1);
+            const int bh = q / npairs, pp = q - bh * npairs;
+            const size_t r0 = (size_t)bh * n + 2 * pp;
+            c0[u] = kv_cnt[r0];
+            c1[u] = kv_cnt[2 * pp + 1 < n ? r0 + 1 : r0];
+        }
+#pragma unroll
+        for (int u = 0; u < FILL; ++u) {
+            const int q = t + u * kPlanThreads;
+            const int pp = q % npairs;
+            const int a = min(max(c0[u], 0), n), b = 2 * pp + 1 < n ? min(max(c1[u], 0), n) : 0;
+            if (q < Pi) cache[q] = (uint32_t)a | ((uint32_t)b << 16);
         }
         __syncthreads();
     }
@@ -365,10 +394,12 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const int32_t* __res
     const long long pre = plan_scan<long long>(mine, scan64, W);
     {
         long long run = pre;
+        int h = h0, pp = p0;
         for (long long q = q0; q < q1; ++q) {
             const Pair c = counts(q);
-            if (q % npairs == 0) hp[q / npairs] = run;
+            if (pp == 0) hp[h] = run;
             run += 4 + c.c0 + c.c1;
+            if (++pp == npairs) { pp = 0; ++h; }
         }
         if (t == 0) hp[BH] = W;
     }
@@ -398,22 +429,54 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const int32_t* __res
             if (cs > n) { cs = 0; break; }
         }
     }
-    // XCD of every pair: its head's cost range, by the pair's midpoint
-    auto xcd_of = [&](long long q, long long before, const Pair& c) {
-        const int h = (int)(q / npairs);
-        const long long tot = hp[h + 1] - hp[h];
-        const long long mid2 = 2 * (before - hp[h]) + 4 + c.c0 + c.c1;
-        return (int)min<long long>(kXcds - 1, (mid2 * kXcds) / (2 * tot));
+    // XCD of every pair: its head's cost range (from hb, tot long), by the
+    // pair's midpoint, min(7, floor(8 mid2 / (2 tot))) counted by comparisons
+    // (a head's cost is at most npairs (4 + 2n) < 2^25, so its midpoints
+    // and their multiples of tot stay inside 32 bits)
+    auto xcd_of = [&](long long hb, long long tot, long long before, const Pair& c) {
+        const int mid4 = 4 * (2 * (int)(before - hb) + 4 + c.c0 + c.c1);
+        const int tt = (int)tot;
+        int xq = 0;
+#pragma unroll
+        for (int k = 1; k < kXcds; ++k) xq += mid4 >= k * tt ? 1 : 0;
+        return xq;
     };
-    long long cntx[kXcds] = {};
+    // the head prefixes of a thread's current head, read again only when
+    // its range crosses into the next head
+    struct HeadWalk {
+        int h, pp;
+        long long hb, tot;
+    };
+    auto head_start = [&]() {
+        HeadWalk hw{h0, p0, 0, 1};
+        if (q0 < q1) {
+            hw.hb = hp[h0];
+            hw.tot = hp[h0 + 1] - hw.hb;
+        }
+        return hw;
+    };
+    auto head_next = [&](HeadWalk& hw, long long q) {
+        if (++hw.pp == npairs) {
+            hw.pp = 0;
+            ++hw.h;
+            if (q + 1 < q1) {
+                hw.hb = hp[hw.h];
+                hw.tot = hp[hw.h + 1] - hw.hb;
+            }
+        }
+    };
+    int cntx[kXcds] = {};
     long long slots_mine = 0, splits_mine = 0;
     {
         long long run = pre;
+        HeadWalk hw = head_start();
         for (long long q = q0; q < q1; ++q) {
             const Pair c = counts(q);
-            const int xq = xcd_of(q, run, c);
+            const int xq = xcd_of(hw.hb, hw.tot, run, c);
+            head_next(hw, q);
             const long long C = nchunks(c, cs);
-            cntx[xq] += C;
+#pragma unroll
+            for (int xx = 0; xx < kXcds; ++xx) cntx[xx] += xx == xq ? (int)C : 0;
             if (C > 1) {
                 slots_mine += C;
                 splits_mine += 1;
@@ -424,22 +487,24 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const int32_t* __res
     if (t < kXcds) xcnt[t] = 0;
     __syncthreads();
     for (int xx = 0; xx < kXcds; ++xx)
-        if (cntx[xx]) atomicAdd(&xcnt[xx], (int)cntx[xx]);
+        if (cntx[xx]) atomicAdd(&xcnt[xx], cntx[xx]);
     __syncthreads();
     int first = 0;
     for (int xx = 0; xx < x; ++xx) first += xcnt[xx];
     const int lenx = xcnt[x];
     long long dummy = 0;
-    const long long posx = plan_scan<long long>(cntx[x], scan64, dummy);
+    const long long posx = plan_scan<long long>((long long)cntx[x], scan64, dummy);
     const long long slot0 = plan_scan<long long>(slots_mine, scan64, dummy);
     long long nsplit = 0;
     const long long split0 = plan_scan<long long>(splits_mine, scan64, nsplit);
     // this XCD's items, head-major; the chunks of a split pair described
     {
         long long run = pre, pos = first + posx, slot = slot0, sidx = split0;
+        HeadWalk hw = head_start();
         for (long long q = q0; q < q1; ++q) {
             const Pair c = counts(q);
-            const int xq = xcd_of(q, run, c);
+            const int xq = xcd_of(hw.hb, hw.tot, run, c);
+            head_next(hw, q);
             const long long C = nchunks(c, cs);
             if (C == 1) {
                 if (xq == x) pl.items[pos++] = (int)q;
@@ -493,13 +558,12 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const int32_t* __res
         atomicAdd(&cursor[bucket(it)], 1);
     }
     __syncthreads();
-    if (t == 0) {   // exclusive scan of the bucket sizes (kPlanBuckets entries)
-        int run = 0;
-        for (int bb = 0; bb < kPlanBuckets; ++bb) {
-            const int c = cursor[bb];
-            cursor[bb] = run;
-            run += c;
-        }
+    {   // exclusive scan of the bucket sizes (kPlanBuckets <= kPlanThreads entries)
+        static_assert(kPlanBuckets <= kPlanThreads, "one bucket per thread");
+        const int c = t < kPlanBuckets ? cursor[t] : 0;
+        int all = 0;
+        const int ex = plan_scan<int>(c, scan32, all);
+        if (t < kPlanBuckets) cursor[t] = ex;
     }
     __syncthreads();
     for (int a = t; a < lenx; a += kPlanThreads) {
