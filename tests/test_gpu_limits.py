@@ -10,6 +10,9 @@
   tail block) with rows that keep every block, long random lists, and short
   lists is checked on sampled query blocks: every full row, the first and
   the tail block, and a few others.
+* The work plan keeps the counts of up to 16384 pairs in LDS; a layer of
+  40 heads x 1024 blocks (20480 pairs) takes its path that reads them from
+  memory.
 """
 import math
 
@@ -104,6 +107,54 @@ def test_attention_at_max_blocks():
         Oo, Lo = O.attention(qf, kf, vf, rows[h], cfg.block, scale, rows=sample)
         for i in sample:
             sl = slice(i * cfg.block, min(cfg.L, (i + 1) * cfg.block))
+            mx, mean = attention_errors(og[0, h, sl], Oo[sl])
+            assert mx <= MAX_ABS and mean <= MEAN_ABS, (h, i, mx, mean)
+            assert np.abs(lg[0, h, sl] - Lo[sl]).max() <= LSE_ABS, (h, i)
+
+
+def test_attention_plan_beyond_count_cache():
+    """The work plan keeps both counts of up to 16384 pairs in LDS and reads
+    them from memory beyond that; every other test stays below.  40 heads of
+    1024 blocks (20480 pairs), each row a band of five blocks around the
+    diagonal plus 0–40 seeded random blocks, heads of uneven cost (the
+    random part grows with the head index), sampled query blocks of three
+    heads against the oracle."""
+    H, L, d, bs = 40, 65536, 64, 64
+    n = L // bs
+    assert H * ((n + 1) // 2) > 16384
+    rng = np.random.default_rng(31)
+    host = tuple(W.to_bf16_bits(rng.standard_normal((1, H, L, d)).astype(np.float32)) for _ in range(3))
+    qd, kd, vd = (bf16_tensor(x) for x in host)
+    shape = M.make_shape(1, H, L, d, bs, L)
+    assert M.mod_num_blocks(shape) == n
+    rows = []
+    for h in range(H):
+        rh = []
+        for i in range(n):
+            band = set(range(max(0, i - 2), min(n, i + 3)))
+            extra = rng.integers(0, n, size=int(rng.integers(0, 1 + h)))
+            rh.append(sorted(band | set(extra.tolist())))
+        rows.append(rh)
+    idx = np.zeros((1, H, n, n), np.int32)
+    cnt = np.zeros((1, H, n), np.int32)
+    for h in range(H):
+        for i, js in enumerate(rows[h]):
+            cnt[0, h, i] = len(js)
+            idx[0, h, i, :len(js)] = js
+    o = torch.empty_like(qd)
+    lse = torch.empty((1, H, L), dtype=torch.float32, device="cuda")
+    M.mod_block_sparse_attn_fwd(shape, qd, kd, vd, torch.from_numpy(idx).cuda(), torch.from_numpy(cnt).cuda(),
+                                0.0, o, lse)
+    torch.cuda.synchronize()
+    og = bf16_to_f64(o)
+    lg = lse.cpu().numpy().astype(np.float64)
+    scale = 1.0 / math.sqrt(d)
+    sample = [0, 1, 2, 255, 511, 512, 777, n - 2, n - 1]
+    for h in (0, 17, H - 1):
+        qf, kf, vf = (W.bf16_bits_to_f64(x[0, h]) for x in host)
+        Oo, Lo = O.attention(qf, kf, vf, rows[h], bs, scale, rows=sample)
+        for i in sample:
+            sl = slice(i * bs, (i + 1) * bs)
             mx, mean = attention_errors(og[0, h, sl], Oo[sl])
             assert mx <= MAX_ABS and mean <= MEAN_ABS, (h, i, mx, mean)
             assert np.abs(lg[0, h, sl] - Lo[sl]).max() <= LSE_ABS, (h, i)
