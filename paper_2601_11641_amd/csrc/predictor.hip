@@ -536,17 +536,14 @@ __global__ __launch_bounds__(kThreads) void extrapolate_kernel(const double* __r
 
 // ---------------------------------------------------------------------------
 // a5: per-row selection.  One wave per (head, query block i) up to n = 1024
-// (select_wave_kernel, a threshold search), one work-group of 256 threads per
-// row above (select_kernel, a sort).
+// (select_wave_kernel), one work-group of 256 threads per row above
+// (select_kernel), both by the same threshold search.
 //   sigma_j = n (c~[j-i] + d~[j]) in fp64, rounded to float: the ranking key.
 //   The non-forced blocks are ranked by (sigma desc, j asc).  TOPK keeps the
 //   first max(0, k - |forced|) of them; MASS keeps the shortest prefix whose
 //   positive key mass, added to the forced blocks' mass, reaches tau of the
 //   row total (fp64 sums; at least one block).  The kept set is compacted in
 //   ascending j.
-//   select_kernel gives every non-forced block the 64-bit key
-//   (order(sigma) << 32 | ~j) and sorts descending (bitonic), forced blocks
-//   and padding with key 0 last, and takes prefix sums in sorted order.
 // With a text segment after the video (token-type-aware masking) n counts
 // the video blocks, the lists have ldn >= n entries per row, the block tb0
 // shared by the video and the text (tb0 < n) is forced, and every row keeps
@@ -560,213 +557,6 @@ __device__ inline uint32_t order_bits(float f) {
 __device__ inline float order_bits_to_float(uint32_t k) {
     const uint32_t u = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
     return __uint_as_float(u);
-}
-
-// x of lane l ^ mask.  Masks 1 and 2 stay within a quad and 8 within a
-// row of 16 lanes (a rotation by 8), so they move through the DPP network
-// at no memory-pipeline cost; 32 swaps the wave's halves
-// (v_permlane32_swap with x in both operands returns x[l mod 32] and
-// x[l mod 32 + 32] to lane l); other masks use the LDS crossbar.
-template <bool kDpp>
-__device__ inline uint32_t xchg_u32(uint32_t x, int mask) {
-    if (!kDpp) return (uint32_t)__shfl_xor((int)x, mask);
-    switch (mask) {
-        case 1: return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, false);   // quad_perm 1,0,3,2
-        case 2: return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x4E, 0xF, 0xF, false);   // quad_perm 2,3,0,1
-        case 8: return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x128, 0xF, 0xF, false);  // row_ror:8
-        case 32: {
-            const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
-            return (threadIdx.x & 32) ? r[0] : r[1];
-        }
-        default: return (uint32_t)__shfl_xor((int)x, mask);
-    }
-}
-
-template <bool kDpp>
-__device__ inline uint64_t shfl_xor_u64(uint64_t v, int mask) {
-    const uint32_t lo = xchg_u32<kDpp>(static_cast<uint32_t>(v), mask);
-    const uint32_t hi = xchg_u32<kDpp>(static_cast<uint32_t>(v >> 32), mask);
-    return (static_cast<uint64_t>(hi) << 32) | lo;
-}
-
-// E = npad / kThreads keys per thread: thread t holds positions E*t .. E*t+E-1.
-template <int E>
-__global__ __launch_bounds__(kThreads) void select_kernel(
-    const double* __restrict__ pred, const int32_t* __restrict__ gate,
-    const int* __restrict__ row_lo, const int* __restrict__ row_hi, int mode, int topk,
-    double tau, int32_t* __restrict__ kv_idx, int32_t* __restrict__ kv_cnt, int n,
-    int ldn, int tb0) {
-    constexpr int npad = E * kThreads;
-    extern __shared__ __align__(16) unsigned char smem[];
-    uint64_t* keys = reinterpret_cast<uint64_t*>(smem);          // npad
-    double* scan = reinterpret_cast<double*>(keys + npad);        // npad
-    int* flag = reinterpret_cast<int*>(scan + npad);              // npad
-    __shared__ double red[kThreads];
-    __shared__ double wsum_d[kThreads / 64];
-    __shared__ int wsum_i[kThreads / 64];
-    __shared__ int kk_shared;
-
-    const int row = blockIdx.x;
-    const int bh = row / n, i = row % n;
-    const double* c = pred + (size_t)bh * (3 * n - 1);
-    const double* d = c + (2 * n - 1);
-    const bool g = gate[bh] != 0;
-    const int flo = row_lo[i], fhi = row_hi[i];
-    // forced: the frame blocks of i (gate on) and the block shared by the
-    // video and the text segment (tb0 < n), which is a text block
-    const bool tb_in_frames = g && tb0 >= flo && tb0 <= fhi;
-    const int nf = (g ? (fhi - flo + 1) : 0) + ((tb0 < n && !tb_in_frames) ? 1 : 0);
-    const int n_free = n - nf;
-    const int t = threadIdx.x;
-
-    double forced_mass = 0.0;
-    // thread t starts with the keys of blocks t + 256 e (coalesced loads) at
-    // positions E*t + e; the sort is indifferent to the starting placement
-    uint64_t kr[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        const int j = t + kThreads * e;   // coalesced; the sort places keys by value
-        uint64_t key = 0;
-        int fl = 0;
-        if (j < n) {
-            const double s = static_cast<double>(n) * (c[j - i + n - 1] + d[j]);
-            const float kf = static_cast<float>(s);
-            if ((g && j >= flo && j <= fhi) || j == tb0) {
-                fl = 1;
-                forced_mass += fmax(static_cast<double>(kf), 0.0);
-            } else {
-                key = (static_cast<uint64_t>(order_bits(kf)) << 32) |
-                      static_cast<uint64_t>(0xFFFFFFFFu - static_cast<uint32_t>(j));
-            }
-        }
-        kr[e] = key;
-        flag[j] = fl;
-    }
-
-    // Descending bitonic sort of the npad keys.  Stage (kk, jj) pairs
-    // positions a and a ^ jj; the lower position of a pair keeps the larger
-    // key when (a & kk) == 0, the smaller one otherwise.  Partners within a
-    // thread (jj < E) are in its registers, within a wave (jj < 64 E) they
-    // are exchanged by cross-lane shuffles, and only the stages with partners
-    // in other waves go through LDS.
-#pragma unroll
-    for (int kk = 2; kk <= npad; kk <<= 1) {
-#pragma unroll
-        for (int jj = kk >> 1; jj > 0; jj >>= 1) {
-            if (jj < E) {
-#pragma unroll
-                for (int e = 0; e < E; ++e) {
-                    const int eb = e ^ jj;
-                    if (eb > e) {
-                        const int a = E * t + e;
-                        const bool desc = (a & kk) == 0;
-                        const uint64_t ka = kr[e], kb = kr[eb];
-                        const bool swap = desc ? (ka < kb) : (ka > kb);
-                        kr[e] = swap ? kb : ka;
-                        kr[eb] = swap ? ka : kb;
-                    }
-                }
-            } else {
-                uint64_t pv[E];
-                if (jj < 64 * E) {
-#pragma unroll
-                    for (int e = 0; e < E; ++e) pv[e] = shfl_xor_u64<(E <= 8)>(kr[e], jj / E);
-                } else {
-                    __syncthreads();     // the previous exchange has been read
-#pragma unroll
-                    for (int e = 0; e < E; ++e) keys[E * t + e] = kr[e];
-                    __syncthreads();
-#pragma unroll
-                    for (int e = 0; e < E; ++e) pv[e] = keys[(E * t + e) ^ jj];
-                }
-#pragma unroll
-                for (int e = 0; e < E; ++e) {
-                    const int a = E * t + e;
-                    const bool lower = (a & jj) == 0;
-                    const bool desc = (a & kk) == 0;
-                    const uint64_t hi = kr[e] > pv[e] ? kr[e] : pv[e];
-                    const uint64_t lo = kr[e] > pv[e] ? pv[e] : kr[e];
-                    kr[e] = (lower == desc) ? hi : lo;
-                }
-            }
-        }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int e = 0; e < E; ++e) keys[E * t + e] = kr[e];
-    __syncthreads();
-
-    int keep;
-    if (mode == 0) {
-        keep = min(n_free, max(0, topk - nf));
-    } else {
-        const double fm = block_sum(forced_mass, red);
-        // inclusive scan of the positive masses in sorted order
-        double run = 0.0;
-        for (int e = 0; e < E; ++e) {
-            const int pos = t * E + e;
-            const double v =
-                pos < n_free
-                    ? fmax(static_cast<double>(order_bits_to_float(
-                               static_cast<uint32_t>(keys[pos] >> 32))),
-                           0.0)
-                    : 0.0;
-            run += v;
-            scan[pos] = run;
-        }
-        double unused;
-        const double off = block_exclusive_scan(run, wsum_d, &unused);
-        for (int e = 0; e < E; ++e) scan[t * E + e] += off;
-        if (t == 0) kk_shared = n_free;
-        __syncthreads();
-        const double total = fm + scan[npad - 1];
-        const double target = tau * total;
-        const int kmin = nf > 0 ? 0 : 1;
-        for (int e = 0; e < E; ++e) {
-            const int cand = t * E + e;     // keep `cand` free blocks
-            if (cand < kmin || cand > n_free) continue;
-            const double cum = fm + (cand == 0 ? 0.0 : scan[cand - 1]);
-            if (cum >= target) atomicMin(&kk_shared, cand);
-        }
-        __syncthreads();
-        keep = kk_shared;
-    }
-    for (int a = t; a < keep; a += kThreads) {
-        const uint32_t j = 0xFFFFFFFFu - static_cast<uint32_t>(keys[a] & 0xFFFFFFFFull);
-        flag[j] = 1;
-    }
-    __syncthreads();
-
-    // compaction in ascending j
-    int cnt = 0;
-    for (int e = 0; e < E; ++e) cnt += flag[t * E + e];
-    int total;
-    int pos = block_exclusive_scan(cnt, wsum_i, &total);
-    const size_t orow = (size_t)bh * ldn + i;     // row of the [BH, ldn, ldn] lists
-    int32_t* out = kv_idx + orow * ldn;
-    for (int e = 0; e < E; ++e) {
-        const int j = t * E + e;
-        if (flag[j]) out[pos++] = j;
-    }
-    // text blocks after the video blocks: kept in every row
-    for (int j = n + t; j < ldn; j += kThreads) out[total + (j - n)] = j;
-    if (t == 0) kv_cnt[orow] = total + (ldn - n);
-}
-
-
-template <class T>
-__device__ inline T wave_inclusive_scan(T v, int lane) {
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const T y = __shfl_up(v, off);
-        if (lane >= off) v += y;
-    }
-    return v;
-}
-
-__device__ inline void wave_sync_lds() {
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
 }
 
 // The wave's total of a per-lane double in a fixed order, the same bits in
@@ -802,6 +592,183 @@ __device__ inline double wave_total_f64(double v) {
     v += dpp_f64(v, 2);
     v += dpp_f64(v, 3);
     return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
+}
+
+// The same selection with one 256-thread work-group per row (n <= 256 E),
+// E keys per thread (blocks t + 256 e, coalesced), by the threshold search of
+// select_wave_kernel below: each step's count or fp64 sum is taken per wave
+// (scalar counts of 64-lane masks; the fixed-order wave total) and over the
+// four waves in wave order, so every thread holds the same bits.
+template <int E>
+__global__ __launch_bounds__(kThreads) void select_kernel(
+    const double* __restrict__ pred, const int32_t* __restrict__ gate,
+    const int* __restrict__ row_lo, const int* __restrict__ row_hi, int mode, int topk,
+    double tau, int32_t* __restrict__ kv_idx, int32_t* __restrict__ kv_cnt, int n,
+    int ldn, int tb0) {
+    constexpr int NW = kThreads / 64;
+    static_assert(NW == 4, "the wave totals are added as (w0 + w1) + (w2 + w3)");
+    extern __shared__ __align__(16) unsigned char smem[];
+    int* flag = reinterpret_cast<int*>(smem);                     // npad
+    __shared__ double wsum_d[NW];
+    __shared__ int wsum_i[NW];
+
+    const int row = blockIdx.x;
+    const int bh = row / n, i = row % n;
+    const double* c = pred + (size_t)bh * (3 * n - 1);
+    const double* d = c + (2 * n - 1);
+    const bool g = gate[bh] != 0;
+    const int flo = row_lo[i], fhi = row_hi[i];
+    // forced: the frame blocks of i (gate on) and the block shared by the
+    // video and the text segment (tb0 < n), which is a text block
+    const bool tb_in_frames = g && tb0 >= flo && tb0 <= fhi;
+    const int nf = (g ? (fhi - flo + 1) : 0) + ((tb0 < n && !tb_in_frames) ? 1 : 0);
+    const int n_free = n - nf;
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+
+    double forced_mass = 0.0;
+    uint32_t vb[E];
+    double ms[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int j = t + kThreads * e;   // coalesced
+        vb[e] = 0;
+        ms[e] = 0.0;
+        int fl = 0;
+        if (j < n) {
+            const double sv = static_cast<double>(n) * (c[j - i + n - 1] + d[j]);
+            const float kf = static_cast<float>(sv);
+            if ((g && j >= flo && j <= fhi) || j == tb0) {
+                fl = 1;
+                forced_mass += fmax(static_cast<double>(kf), 0.0);
+            } else {
+                vb[e] = order_bits(kf);
+                ms[e] = fmax(static_cast<double>(kf), 0.0);
+            }
+        }
+        flag[j] = fl;
+    }
+    auto total_f64 = [&](double v) {    // over the work-group, fixed order
+        v = wave_total_f64(v);
+        if (lane == 0) wsum_d[w] = v;
+        __syncthreads();
+        const double tot = (wsum_d[0] + wsum_d[1]) + (wsum_d[2] + wsum_d[3]);
+        __syncthreads();
+        return tot;
+    };
+    auto count_ge = [&](uint32_t th) {  // free keys with bits >= th (th >= 1)
+        int cnt = 0;
+#pragma unroll
+        for (int e = 0; e < E; ++e) cnt += __popcll(__ballot(vb[e] >= th));
+        if (lane == 0) wsum_i[w] = cnt;
+        __syncthreads();
+        const int tot = (wsum_i[0] + wsum_i[1]) + (wsum_i[2] + wsum_i[3]);
+        __syncthreads();
+        return tot;
+    };
+    auto mass_ge = [&](uint32_t th) {   // their mass (th >= 1)
+        double sm = 0.0;
+#pragma unroll
+        for (int e = 0; e < E; ++e) sm += vb[e] >= th ? ms[e] : 0.0;
+        return total_f64(sm);
+    };
+
+    uint32_t p;     // boundary bits
+    int r;          // keys kept at the boundary, in ascending j
+    int keep = -1;  // free keys kept, when found by count
+    if (mode == 0) {
+        keep = min(n_free, max(0, topk - nf));
+    } else {
+        const double fm = total_f64(forced_mass);
+        const double total = fm + (n_free > 0 ? mass_ge(1u) : 0.0);
+        const double target = tau * total;
+        const int kmin = nf > 0 ? 0 : 1;
+        if (fm >= target) {
+            keep = min(n_free, kmin);
+        } else if (total < target) {
+            keep = n_free;
+        } else {
+            p = 0x80000000u;   // the boundary key has a positive mass
+            for (int b = 30; b >= 0; --b) {
+                const uint32_t th = p | (1u << b);
+                if (fm + mass_ge(th) >= target) p = th;
+            }
+            const double hi = fm + (p < 0xFFFFFFFFu ? mass_ge(p + 1) : 0.0);
+            const int ties = count_ge(p) - (p < 0xFFFFFFFFu ? count_ge(p + 1) : 0);
+            const double mp = fmax(static_cast<double>(order_bits_to_float(p)), 0.0);
+            r = 1;
+            while (r < ties && hi + static_cast<double>(r) * mp < target) ++r;
+        }
+    }
+    if (keep >= 0) {
+        if (keep == 0) {
+            p = 0xFFFFFFFFu;
+            r = 0;
+        } else if (keep >= n_free) {
+            p = 0;
+            r = 0;
+        } else {
+            p = 0;
+            for (int b = 31; b >= 0; --b) {
+                const uint32_t th = p | (1u << b);
+                if (count_ge(th) >= keep) p = th;
+            }
+            r = keep - (p < 0xFFFFFFFFu ? count_ge(p + 1) : 0);
+        }
+    }
+    // flags: 1 kept, 2 at the boundary (resolved below in ascending j)
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int j = t + kThreads * e;
+        if (vb[e] > p)
+            flag[j] = 1;
+        else if (vb[e] == p && vb[e] != 0)
+            flag[j] = 2;
+    }
+    __syncthreads();
+    int f[E];
+    int nt = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        f[e] = flag[t * E + e];
+        nt += f[e] == 2;
+    }
+    int ntie;
+    int tr = block_exclusive_scan(nt, wsum_i, &ntie);   // boundary keys before this thread
+    int cnt = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        if (f[e] == 2) f[e] = tr++ < r ? 1 : 0;
+        cnt += f[e];
+    }
+
+    // compaction in ascending j
+    int total;
+    int pos = block_exclusive_scan(cnt, wsum_i, &total);
+    const size_t orow = (size_t)bh * ldn + i;     // row of the [BH, ldn, ldn] lists
+    int32_t* out = kv_idx + orow * ldn;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int j = t * E + e;
+        if (f[e]) out[pos++] = j;
+    }
+    // text blocks after the video blocks: kept in every row
+    for (int j = n + t; j < ldn; j += kThreads) out[total + (j - n)] = j;
+    if (t == 0) kv_cnt[orow] = total + (ldn - n);
+}
+
+template <class T>
+__device__ inline T wave_inclusive_scan(T v, int lane) {
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const T y = __shfl_up(v, off);
+        if (lane >= off) v += y;
+    }
+    return v;
+}
+
+__device__ inline void wave_sync_lds() {
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
 }
 
 // One wave per row (n <= 64 EW).  Every free block j holds its ranking key
@@ -1188,12 +1155,8 @@ hipError_t launch_select(const double* pred, const int32_t* gate, const int* row
     }
     int npad = kThreads;
     while (npad < n) npad <<= 1;
-    const size_t lds = (size_t)npad * (sizeof(uint64_t) + sizeof(double) + sizeof(int));
+    const size_t lds = (size_t)npad * sizeof(int);
     auto go = [&](auto kern) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)((size_t)kMaxBlocks * 20));
-        if (e != hipSuccess) return e;
         hipLaunchKernelGGL(kern, dim3((unsigned)BH * n), dim3(kThreads), lds, s, pred, gate, row_lo, row_hi,
                            mode, k, tau, kv_idx, kv_cnt, n, ldn, tb0);
         return hipGetLastError();

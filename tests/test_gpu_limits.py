@@ -21,7 +21,7 @@ import pytest
 
 import oracle as O
 import workloads as W
-from parity import LSE_ABS, MAX_ABS, MEAN_ABS, attention_errors, bf16_tensor, bf16_to_f64
+from parity import LSE_ABS, MAX_ABS, MEAN_ABS, attention_errors, bf16_tensor, bf16_to_f64, gpu_lists
 
 import paper_2601_11641_amd as M
 from test_gpu_parity import _check_predictor, _run_predictor
@@ -55,6 +55,32 @@ def test_select_register_widths(name, budget):
     dev = tuple(bf16_tensor(x) for x in host)
     params = dict(warmup_m=1, delta_t=0)
     st, kv_idx, kv_cnt, P, sel, qf, kf = _run_predictor(cfg, dev, host, [1], 2, budget, params)
+    _check_predictor(cfg, st, kv_idx, kv_cnt, P, sel, qf, kf, budget, 2)
+    st.close()
+
+
+@pytest.mark.parametrize("budget", [("topk", 0.2), ("mass", 0.7)])
+@pytest.mark.parametrize("tau_e", [-1.0, 1.0])
+def test_select_tied_scores_work_group(budget, tau_e):
+    """The one-work-group-per-row selection (n > 1024) on tied scores: every Q
+    token and every K token the same vector, so a row's scores take one or
+    two float32 values and the lists rest on the tie rule (ascending j), the
+    frame blocks forced (tau_e below the zero frame energy) or not."""
+    cfg = SELECT["n1172"]
+    q, k, v = W.generate(cfg)
+    q = np.ascontiguousarray(np.broadcast_to(q[:, :, :1, :], q.shape))
+    k = np.ascontiguousarray(np.broadcast_to(k[:, :, :1, :], k.shape))
+    host = (q, k, v)
+    dev = tuple(bf16_tensor(x) for x in host)
+    params = dict(warmup_m=1, delta_t=0, tau_e=tau_e)
+    st, kv_idx, kv_cnt, P, sel, qf, kf = _run_predictor(cfg, dev, host, [1], 2, budget, params)
+    assert P.gates.all() == (tau_e < 0) and P.gates.any() == (tau_e < 0)
+    ct, dt_ = P.prediction(2)[0][0]
+    keys = O.scores(ct, dt_, st.n).astype(np.float32)
+    assert max(len(set(r.tolist())) for r in keys) <= 2      # the ties are there
+    rows = gpu_lists(kv_idx, kv_cnt)
+    for i in range(st.n):
+        assert rows[0][0][i] == sel[0][0][i].kept.tolist(), i
     _check_predictor(cfg, st, kv_idx, kv_cnt, P, sel, qf, kf, budget, 2)
     st.close()
 
